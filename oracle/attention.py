@@ -1,0 +1,139 @@
+"""fp64 reference for causal prefill of a suffix over a cached prefix.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Definition followed (paper Sec. 1 and 2.1; Sec. 3.3 after Eq. 1): prefix
+caching reuses the KV states of the leading P tokens of a prompt, so only the S
+suffix tokens are prefilled, and the result must equal what a from-scratch
+prefill of all P + S tokens gives for those rows: prefix reuse changes cost,
+not what the model sees. The paper does not write out the attention itself; it
+is standard scaled-dot-product causal attention over the serving engine's KV
+blocks. The readings taken here:
+
+* suffix row i sits at absolute position P + i and sees keys 0 .. P + i
+  (bottom-right alignment of the causal mask);
+* grouped-query attention with contiguous groups: query head h reads KV head
+  h // (Hq / Hkv);
+* softmax scale is an explicit argument (1/sqrt(D) in every workload);
+* inputs are the logical sequences (never a device cache); every value is
+  upcast exactly to float64 and the result is returned in float64.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+def _as_f64(x) -> np.ndarray:
+    """Exact upcast of a float array (numpy or torch, any float dtype) to float64."""
+    if hasattr(x, "detach"):  # torch tensor; bf16 has no numpy dtype
+        x = x.detach().to("cpu").double().numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def suffix_prefill_attention(q, k, v, prefix_len: int, scale: float,
+                             row_chunk: int = 256) -> np.ndarray:
+    """Attention output of the S suffix rows of one request.
+
+    q: [S, Hq, D] suffix queries; k, v: [L, Hkv, D] logical keys/values of the
+    whole prompt (L = prefix_len + S, prefix first). Returns [S, Hq, D] float64.
+
+    For each query head h (KV head g = h // G) and suffix row i:
+        s_j = scale * <q[i, h], k[j, g]>           for j = 0 .. prefix_len + i
+        O[i, h] = sum_j exp(s_j - max s) v[j, g] / sum_j exp(s_j - max s)
+    Rows are processed in chunks of `row_chunk` only to bound memory; each row's
+    arithmetic is independent of the chunking.
+    """
+    q = _as_f64(q)
+    k = _as_f64(k)
+    v = _as_f64(v)
+    S, Hq, D = q.shape
+    L, Hkv, Dk = k.shape
+    if Dk != D or v.shape != k.shape:
+        raise ValueError("k/v shape mismatch")
+    if L != prefix_len + S:
+        raise ValueError(f"logical length {L} != prefix {prefix_len} + suffix {S}")
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = Hq // Hkv
+    out = np.zeros((S, Hq, D), dtype=np.float64)
+    if S == 0:
+        return out
+    key_pos = np.arange(L)
+    for g in range(Hkv):
+        kg = k[:, g, :]                      # [L, D]
+        vg = v[:, g, :]                      # [L, D]
+        for r0 in range(0, S, row_chunk):
+            r1 = min(S, r0 + row_chunk)
+            qg = q[r0:r1, g * G:(g + 1) * G, :]          # [R, G, D]
+            scores = scale * (qg @ kg.T)                   # [R, G, L]
+            row_pos = prefix_len + np.arange(r0, r1)       # absolute positions
+            visible = key_pos[None, :] <= row_pos[:, None]  # [R, L]
+            scores = np.where(visible[:, None, :], scores, -np.inf)
+            m = scores.max(axis=2, keepdims=True)
+            w = np.exp(scores - m)                         # exp(-inf) = 0
+            out[r0:r1, g * G:(g + 1) * G, :] = (w @ vg) / w.sum(axis=2, keepdims=True)
+    return out
+
+
+def suffix_prefill_attention_loops(q, k, v, prefix_len: int, scale: float) -> np.ndarray:
+    """The same definition written as plain Python loops (tiny inputs only)."""
+    q = _as_f64(q)
+    k = _as_f64(k)
+    v = _as_f64(v)
+    S, Hq, D = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    out = np.zeros((S, Hq, D), dtype=np.float64)
+    for i in range(S):
+        pos = prefix_len + i
+        for h in range(Hq):
+            g = h // G
+            s = []
+            for j in range(pos + 1):
+                acc = 0.0
+                for d in range(D):
+                    acc += float(q[i, h, d]) * float(k[j, g, d])
+                s.append(scale * acc)
+            m = max(s)
+            w = [math.exp(x - m) for x in s]
+            tot = sum(w)
+            for d in range(D):
+                acc = 0.0
+                for j in range(pos + 1):
+                    acc += w[j] * float(v[j, g, d])
+                out[i, h, d] = acc / tot
+    return out
+
+
+def batch_suffix_prefill_attention(qs, ks, vs, prefix_lens, scale: float) -> list:
+    """Per-request outputs for a ragged batch (lists of per-request arrays)."""
+    return [suffix_prefill_attention(q, k, v, p, scale)
+            for q, k, v, p in zip(qs, ks, vs, prefix_lens)]
+
+
+def suffix_prefill_rows(q, k, v, prefix_len: int, scale: float, rows) -> np.ndarray:
+    """Output of selected suffix rows only: [len(rows), Hq, D] float64.
+
+    Each row depends only on its own query and keys 0 .. prefix_len + row, so a
+    sampled row is computed exactly as in the full call.
+    """
+    q = _as_f64(q)
+    rows = np.asarray(rows, dtype=np.int64)
+    res = np.zeros((len(rows), q.shape[1], q.shape[2]), dtype=np.float64)
+    kf = _as_f64(k)
+    vf = _as_f64(v)
+    for n, i in enumerate(rows):
+        L = prefix_len + int(i) + 1
+        res[n] = suffix_prefill_attention(q[i:i + 1], kf[:L], vf[:L], prefix_len + int(i), scale)[0]
+    return res
+
+
+def attention_flops(prefix_lens, suffix_lens, num_q_heads: int, head_dim: int) -> int:
+    """Algorithmic FLOPs of the visible (query, key) pairs: QK^T and PV
+    multiply-adds, 4 * D * Hq * sum_r (S_r * P_r + S_r (S_r + 1) / 2)."""
+    pairs = 0
+    for p, s in zip(prefix_lens, suffix_lens):
+        pairs += s * p + s * (s + 1) // 2
+    return 4 * head_dim * num_q_heads * pairs
