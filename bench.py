@@ -1,0 +1,279 @@
+"""Throughput of suffix prefill over paged cached prefixes on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+Workload (default): a batch of 16 concurrent requests from a synthetic RAG
+trace (pool of 200 chunks of 256 tokens, top-5 retrieval, 3 of 5 chunks shared
+with the previous query, evidence ordered by the greedy knowledge-tree walk,
+64-token instruction and question, 1408-token prompts) with Llama-3-8B-shaped
+attention (32 query heads, 8 KV heads, head_dim 128, 16-token blocks, bf16).
+The requests' cached depths are whatever the block pool matches after 64
+warm-up queries were served.
+
+One step is one pass of the whole path over that batch:
+  host   clone the pool state, cw_schedule_batch (chained hashes, prefix match,
+         allocation, commit), cw_suffix_prefill_plan, async copy of the block
+         table / offsets / plan through pinned buffers;
+  device cw_kv_append, then cw_suffix_prefill_attn (one attention layer);
+  host   cw_release_batch.
+Inputs (Q and the new K/V rows, the cached prefix blocks) are resident in HBM
+before timing starts. K steps are timed between two device synchronisations;
+the attention kernel is also timed on its own with HIP events on its stream.
+
+Prints one JSON line. `value` is attention TFLOP/s over the whole step
+(algorithmic FLOPs 4 * D * Hq * sum_r (S_r P_r + S_r (S_r + 1) / 2)).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def attention_flops(prefix_len, suffix_len, hq, d) -> int:
+    pairs = sum(int(s) * int(p) + int(s) * (int(s) + 1) // 2 for p, s in zip(prefix_len, suffix_len))
+    return 4 * d * hq * pairs
+
+
+def attention_bytes(prefix_len, suffix_len, hq, hkv, d) -> int:
+    """Algorithmic HBM bytes of one attention launch: Q read and O written once,
+    every request's K and V read once (prefix and suffix)."""
+    tot = 0
+    for p, s in zip(prefix_len, suffix_len):
+        tot += 2 * s * hq * d * 2 + 2 * (p + s) * hkv * d * 2
+    return tot
+
+
+def append_bytes(suffix_len, hkv, d) -> int:
+    """kv_append: read the new K and V rows, write them into the cache."""
+    return 2 * 2 * int(sum(suffix_len)) * hkv * d * 2
+
+
+def make_workload(name: str, seed: int):
+    from paper_2606_19667_amd import workload as W
+    if name == "llama8b-trace-b16":
+        return W.llama8b_trace_batch(seed=seed)
+    if name == "llama8b-single":
+        return W.llama8b_single(seed)
+    if name.startswith("topk10-f"):
+        return W.topk_sweep(float(name[len("topk10-f"):]), seed)
+    if name in ("llama70b-long-low", "llama70b-long-high"):
+        return W.long_context(name.rsplit("-", 1)[1], seed)
+    if name == "tiny":
+        return W.tiny_single(seed)
+    raise SystemExit(f"unknown workload {name}")
+
+
+def cpu_baseline(w, sched, budget_s: float = 12.0):
+    """The fp64 oracle on the host cores over whole requests of the batch, until
+    about `budget_s` seconds have been spent (at least one request)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import attention as OA
+    from paper_2606_19667_amd import batch as B
+
+    cores = len(os.sched_getaffinity(0))
+    db_host = None
+    flops = 0
+    tokens = 0
+    n = 0
+    elapsed = 0.0
+    with threadpool_limits(limits=cores):
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        order = list(range(w.batch))
+        for r in order:
+            from paper_2606_19667_amd.workload import logical_kv, suffix_q
+            P = int(sched.prefix_len[r])
+            k, v = logical_kv(w, w.prompts[r])
+            q = suffix_q(w, w.prompts[r], P)
+            t0 = time.perf_counter()
+            OA.suffix_prefill_attention(q, k, v, P, w.scale)
+            elapsed += time.perf_counter() - t0
+            S = q.shape[0]
+            flops += attention_flops([P], [S], w.num_q_heads, w.head_dim)
+            tokens += S
+            n += 1
+            if elapsed >= budget_s:
+                break
+    del db_host, B
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "sample": f"{n} of {w.batch} requests, all heads and rows, fp64 NumPy",
+            "seconds": round(elapsed, 3), "suffix_tokens_per_s": tokens / elapsed}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="llama8b-trace-b16")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(requests, KV heads or prefix blocks would be sharded across GPUs; "
+              "see the design notes).", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2606_19667_amd import batch as B
+    from paper_2606_19667_amd import cw
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print(f"[bench] setting up {args.workload}", file=sys.stderr, flush=True)
+
+    w = make_workload(args.workload, args.seed)
+    stride = B.bt_stride_for(w)
+    # Pool state after the warm-up queries were served: every step starts from it.
+    snapshot = cw.Pool(w.num_blocks(), w.free_order())
+    for p in w.warmup:
+        bt0, pl0, cu0 = cw.schedule_batch(snapshot, [p.tokens(w.seed)], stride, w.block_size)
+        cw.release_batch(snapshot, bt0, pl0, cu0, w.block_size)
+    batch_tokens = [p.tokens(w.seed) for p in w.prompts]
+    if w.prefix_lens is None:
+        probe = snapshot.clone()
+        sched = B.Scheduled(*cw.schedule_batch(probe, batch_tokens, stride, w.block_size), w.num_blocks())
+        probe.close()
+    else:
+        sched = B.schedule(w)
+    db = B.materialize(w, device=dev, keep_host=[], sched=sched,
+                       gen_device="cuda" if w.num_q_heads * sum(p.length for p in w.prompts) > 2e7 else "cpu")
+    hq, hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
+    S = np.diff(sched.cu_suffix)
+    P = sched.prefix_len
+    flops = attention_flops(P, S, hq, D)
+    total_s = int(S.sum())
+
+    stream = torch.cuda.current_stream()
+    meta = db.meta
+    nt = meta.num_tiles
+    # Device metadata buffers and two sets of pinned staging buffers.
+    dev_bt = meta.bt
+    dev_cu = meta.cu
+    dev_pl = meta.plen
+    dev_plan = meta.plan
+    staging = []
+    for _ in range(2):
+        staging.append({
+            "bt": torch.empty(dev_bt.shape, dtype=torch.int32, pin_memory=True),
+            "cu": torch.empty(dev_cu.shape, dtype=torch.int32, pin_memory=True),
+            "pl": torch.empty(dev_pl.shape, dtype=torch.int32, pin_memory=True),
+            "plan": torch.empty(dev_plan.shape, dtype=torch.int32, pin_memory=True),
+            "ev": None,
+        })
+    trace_mode = w.prefix_lens is None
+    ev_attn = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+    ev_app = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+
+    def step(i: int, timed: bool):
+        st = staging[i % 2]
+        if st["ev"] is not None:
+            st["ev"].synchronize()
+        if trace_mode:
+            pool = snapshot.clone()
+            bt, pl, cu = cw.schedule_batch(pool, batch_tokens, stride, w.block_size)
+        else:
+            pool, bt, pl, cu = None, sched.block_table, sched.prefix_len, sched.cu_suffix
+        m = cw.BatchMeta(bt, cu, pl, hq, hkv, D, device=None)
+        if m.num_tiles != nt:
+            raise RuntimeError("the batch changed between steps")
+        st["bt"].numpy()[...] = bt
+        st["cu"].numpy()[...] = cu
+        st["pl"].numpy()[...] = pl
+        st["plan"].numpy()[...] = m.plan_host
+        dev_bt.copy_(st["bt"], non_blocking=True)
+        dev_cu.copy_(st["cu"], non_blocking=True)
+        dev_pl.copy_(st["pl"], non_blocking=True)
+        dev_plan.copy_(st["plan"], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        st["ev"] = ev
+        m.bt, m.cu, m.plen, m.plan = dev_bt, dev_cu, dev_pl, dev_plan
+        if timed:
+            ev_app[i][0].record(stream)
+        cw.kv_append(m, db.k_new, db.v_new, db.k_cache, db.v_cache, stream=stream)
+        if timed:
+            ev_app[i][1].record(stream)
+            ev_attn[i][0].record(stream)
+        cw.suffix_prefill_attn(m, db.q, db.k_cache, db.v_cache, w.scale, out=out, stream=stream)
+        if timed:
+            ev_attn[i][1].record(stream)
+        if pool is not None:
+            cw.release_batch(pool, bt, pl, cu, w.block_size)
+            pool.close()
+
+    out = torch.empty_like(db.q)
+    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i, False)
+    torch.cuda.synchronize()
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in ev_attn]))
+    app_ms = float(np.mean([a.elapsed_time(b) for a, b in ev_app]))
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    res = {
+        "metric": "suffix-prefill attention TFLOP/s (whole step: schedule + kv_append + attention)",
+        "value": round(flops / (ms_per_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "num_q_heads": hq, "num_kv_heads": hkv,
+                   "head_dim": D, "block_size": w.block_size, "suffix_tokens": total_s,
+                   "prefix_tokens": int(P.sum()), "prompt_tokens": int(P.sum()) + total_s,
+                   "prefix_len": [int(x) for x in P]},
+        "suffix_tokens_per_s": round(total_s / (ms_per_step * 1e-3), 1),
+        "pct_bf16_peak_step": round(100 * flops / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "attention_us": round(attn_ms * 1e3, 2),
+        "kv_append_us": round(app_ms * 1e3, 2),
+        "kv_append_GBps": round(append_bytes(S, hkv, D) / (app_ms * 1e-3) / 1e9, 1),
+        "attention_GFLOP": round(flops / 1e9, 3),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "suffix_prefill_attn_kernel<128>",
+                     "algorithmic_bytes": attention_bytes(P, S, hq, hkv, D)},
+    }
+    del db
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, sched)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,241 @@
+/*
+ * cw.h - C ABI of libcw: prefill of an uncached prompt suffix over a paged,
+ * prefix-cached KV store, for AMD Instinct MI355X (gfx950).
+ *
+ * The computation is the one that cache-aware evidence ordering shortens
+ * (CacheWeaver, arXiv 2606.19667): a serving engine stores KV states in
+ * fixed-size token blocks, hashes each block together with its prefix history,
+ * reuses the longest leading run of stored blocks of a new prompt, and then
+ * prefills only the remaining suffix tokens, which attend causally over
+ * themselves and fully over the reused prefix (paper Sec. 1; Sec. 2.1 with
+ * Fig. 1; Sec. 3.3, the problem statement after Eq. 1).
+ *
+ * Conventions for every entry point
+ *  - Return value: cw_status. CW_OK on success; on failure nothing observable
+ *    changed (no partial pool update, no kernel launched) and cw_last_error()
+ *    describes the first problem found. No call aborts or throws.
+ *  - Host pointers are read or written only during the call. Device pointers
+ *    are caller-owned HIP device memory; the library never allocates or frees
+ *    device memory and keeps no pointer after returning.
+ *  - Device calls are asynchronous on `stream` (a hipStream_t; NULL = the
+ *    default stream) and do not synchronise. They are reentrant.
+ *  - Pool calls are not thread-safe for one pool; distinct pools are
+ *    independent.
+ *  - Layouts (all row-major, bf16 = IEEE bfloat16 bit patterns):
+ *      q, out        [total_s, Hq, D]        suffix rows of all requests, request-major
+ *      k_new, v_new  [total_s, Hkv, D]
+ *      k_cache,
+ *      v_cache       [num_blocks, Hkv, block_size, D]
+ *      block_table   int32 [batch, bt_stride]; row r lists the physical blocks of
+ *                    request r's logical blocks 0 .. ceil(L_r / block_size) - 1
+ *      cu_suffix     int32 [batch + 1]; request r owns rows cu[r] .. cu[r+1]-1,
+ *                    S_r = cu[r+1] - cu[r] >= 0, cu[0] = 0
+ *      prefix_len    int32 [batch]; P_r cached tokens, a multiple of block_size
+ *    Request r's prompt has L_r = P_r + S_r tokens; suffix row i of request r is
+ *    token P_r + i.
+ *  - Supported shapes: block_size 16, head_dim 64 or 128, num_q_heads a
+ *    multiple of num_kv_heads with at most 128 query heads per KV head.
+ */
+#ifndef CW_H
+#define CW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t cw_status;
+#define CW_OK 0
+#define CW_EINVAL (-1)       /* invalid argument */
+#define CW_EUNSUPPORTED (-2) /* valid but unsupported shape */
+#define CW_ENOSPC (-3)       /* block pool exhausted */
+#define CW_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
+
+#define CW_ABI_VERSION 1
+
+/* ABI version of the loaded library (CW_ABI_VERSION at build time). */
+int32_t cw_abi_version(void);
+
+/* Message describing the last non-OK status returned on the calling thread
+ * (empty string if none). The pointer stays valid until the next cw_ call on
+ * this thread. */
+const char* cw_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Host: chained block hashes (paper Sec. 2.1: each block is hashed together
+ * with its prefix history, so reuse is prefix-sensitive).
+ *
+ * h_b = XXH64(LE32(tokens[b*bs]) .. LE32(tokens[b*bs + bs - 1]), seed = h_{b-1}),
+ * h_{-1} = 0, for the n_tokens / block_size full blocks; a trailing partial
+ * block gets no hash. XXH64 is the published xxHash 64-bit function.
+ *   tokens      host int32 [n_tokens]
+ *   out_hashes  host uint64 [n_tokens / block_size]
+ * CW_EINVAL: n_tokens < 0, block_size < 1, or a needed pointer is NULL.
+ */
+cw_status cw_block_hashes(const int32_t* tokens, int64_t n_tokens, int32_t block_size,
+                          uint64_t* out_hashes);
+
+/* ------------------------------------------------------------------------
+ * Host: block pool (paper Sec. 2.1 and Sec. 3.4: the engine stores KV in
+ * fixed-size blocks, looks up the longest stored prefix, and evicts blocks
+ * itself). The pool keeps only host bookkeeping of block IDs; the KV bytes live
+ * in the caller's device caches.
+ *
+ * Per block: a reference count and at most one stored hash. Blocks with count
+ * zero wait in a free queue; a free block that still stores a hash remains
+ * matchable until it is handed out again (that hand-out evicts the hash).
+ */
+typedef struct cw_pool cw_pool;
+
+/* New pool of `num_blocks` blocks. free_order (host int32 [num_blocks], a
+ * permutation of 0 .. num_blocks-1, or NULL for ascending) is the order in which
+ * never-used blocks are handed out, i.e. the physical placement.
+ * CW_EINVAL: num_blocks < 1, free_order not a permutation, out NULL. */
+cw_status cw_pool_create(int32_t num_blocks, const int32_t* free_order, cw_pool** out);
+
+/* Frees a pool (NULL is ignored). */
+void cw_pool_destroy(cw_pool* pool);
+
+/* Deep copy of a pool's state into a new pool. */
+cw_status cw_pool_clone(const cw_pool* pool, cw_pool** out);
+
+/* Number of blocks whose reference count is zero (-1 if pool is NULL). */
+int32_t cw_pool_num_free(const cw_pool* pool);
+
+/* Longest leading run of `hashes` stored in the pool, at most max_match blocks
+ * (paper Sec. 2.1 and Fig. 1: an early mismatch ends all later reuse). Each
+ * matched block gains one reference (leaving the free queue if it was free).
+ *   hashes         host uint64 [n_hashes]
+ *   out_block_ids  host int32 [n_hashes]; the first *out_depth entries are set
+ *   out_depth      number of matched blocks
+ * Pass max_match = (L - 1) / block_size to keep at least one suffix token.
+ * CW_EINVAL: n_hashes < 0 or a needed pointer is NULL. */
+cw_status cw_prefix_match(cw_pool* pool, const uint64_t* hashes, int32_t n_hashes,
+                          int32_t max_match, int32_t* out_block_ids, int32_t* out_depth);
+
+/* Hands out n blocks from the front of the free queue, each with count 1; a
+ * handed-out block forgets its stored hash.
+ *   out_block_ids  host int32 [n]
+ * CW_ENOSPC: fewer than n free blocks (pool unchanged). CW_EINVAL: n < 0. */
+cw_status cw_pool_alloc(cw_pool* pool, int32_t n, int32_t* out_block_ids);
+
+/* Stores hashes[i] -> block_ids[i] so later prompts can match the block. Each
+ * block must be held (count > 0) and store no other hash. If a hash is already
+ * stored for another block, the pool keeps the first block.
+ * CW_EINVAL: a block not held, out of range, or holding another hash. */
+cw_status cw_pool_commit(cw_pool* pool, const uint64_t* hashes, const int32_t* block_ids,
+                         int32_t n);
+
+/* Drops one reference per listed block. Blocks reaching zero join the back of
+ * the free queue in reverse listing order (the tail of a released sequence is
+ * reused before its head); they keep their hash until handed out again.
+ * CW_EINVAL: a block listed more times than it is held, or out of range. */
+cw_status cw_pool_release(cw_pool* pool, const int32_t* block_ids, int32_t n);
+
+/* One call for a batch of prompts, in order: for each request, chained hashes
+ * of its full blocks, prefix match capped at (L_r - 1) / block_size blocks,
+ * allocation of its remaining ceil(L_r / block_size) - depth blocks, and
+ * commit of the hashes of its new full blocks, so later requests of the same
+ * batch can reuse them (their K/V is written by cw_kv_append of this batch,
+ * which must precede any attention call reading them on the stream).
+ *   tokens            host int32, the prompts concatenated
+ *   cu_tokens         host int64 [batch + 1], prompt r is tokens[cu[r] .. cu[r+1])
+ *   out_block_table   host int32 [batch, bt_stride]; unused entries set to -1
+ *   out_prefix_len    host int32 [batch]   (P_r = depth * block_size)
+ *   out_cu_suffix     host int32 [batch + 1]
+ * On CW_ENOSPC (or any error) every reference taken and hash stored by this
+ * call is undone. CW_EINVAL: empty prompt, ceil(L_r / bs) > bt_stride, or
+ * total suffix rows > INT32_MAX. */
+cw_status cw_schedule_batch(cw_pool* pool, const int32_t* tokens, const int64_t* cu_tokens,
+                            int32_t batch, int32_t block_size, int32_t bt_stride,
+                            int32_t* out_block_table, int32_t* out_prefix_len,
+                            int32_t* out_cu_suffix);
+
+/* Releases every block of every request of a scheduled batch (the first
+ * ceil(L_r / block_size) entries of each row). Arguments as produced by
+ * cw_schedule_batch. */
+cw_status cw_release_batch(cw_pool* pool, const int32_t* block_table, int32_t bt_stride,
+                           const int32_t* prefix_len, const int32_t* cu_suffix, int32_t batch,
+                           int32_t block_size);
+
+/* ------------------------------------------------------------------------
+ * Device: write each request's suffix K and V into its cache blocks (paper
+ * Sec. 2.1: KV memory managed in fixed-size blocks).
+ *
+ * For every request r and token t in [P_r, L_r):
+ *   k_cache[block_table[r, t / bs], h, t % bs, :] = k_new[cu[r] + t - P_r, h, :]
+ * and the same for V; a bit copy. Nothing else in the caches changes. A block
+ * ID outside [0, num_blocks) drops the write (never faults).
+ *   cu_suffix_dev / prefix_len_dev   device copies read by the kernel
+ *   cu_suffix_host / prefix_len_host host copies used for validation and
+ *                                    launch sizing; must hold the same values
+ * CW_EINVAL: NULL pointer, batch < 1, num_kv_heads < 1, P_r % bs != 0,
+ * cu not non-decreasing from 0, ceil(L_r / bs) > bt_stride, num_blocks < 1.
+ * CW_EUNSUPPORTED: head_dim not 64/128 or block_size != 16.
+ * CW_EHIP: launch failure. */
+cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                       const int32_t* block_table, int32_t bt_stride,
+                       const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
+                       const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                       int32_t batch, int32_t num_kv_heads, int32_t head_dim,
+                       int32_t block_size, int32_t num_blocks, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Host: tile schedule for cw_suffix_prefill_attn.
+ *
+ * The attention kernel works on tiles of (request, KV head, run of suffix
+ * rows); the plan lists them heaviest first and groups the tiles of one
+ * (request, KV head) on one L2 partition. A plan depends only on the batch
+ * shape, so one plan serves every layer of a model for that batch.
+ *
+ * cw_suffix_prefill_plan_words returns the int32 capacity a plan needs (or a
+ * negative cw_status). cw_suffix_prefill_plan writes it:
+ *   plan_host       host int32 [plan_words]; copy it to device memory unchanged
+ *   out_num_tiles   number of tile entries to pass to cw_suffix_prefill_attn
+ * CW_EINVAL / CW_EUNSUPPORTED as for cw_suffix_prefill_attn; CW_EINVAL if
+ * plan_words is too small. */
+int64_t cw_suffix_prefill_plan_words(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                     int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                     int32_t head_dim);
+cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                 int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                 int32_t head_dim, int32_t* plan_host, int64_t plan_words,
+                                 int32_t* out_num_tiles);
+
+/* ------------------------------------------------------------------------
+ * Device: causal prefill attention of the suffix rows over the paged prefix
+ * and themselves (paper Sec. 1 and 2.1: with a reused prefix only the suffix is
+ * prefilled, and the result equals a from-scratch prefill of those rows).
+ *
+ * For every request r, query head h (KV head g = h / (Hq / Hkv)) and suffix row
+ * i < S_r, with K_r/V_r the request's logical keys/values read through its
+ * block table (tokens 0 .. L_r - 1):
+ *   s_j = softmax_scale * <q[cu[r] + i, h, :], K_r[j, g, :]>,  j = 0 .. P_r + i
+ *   out[cu[r] + i, h, :] = sum_j softmax(s)_j * V_r[j, g, :]
+ * bf16 inputs, fp32 accumulation and softmax, bf16 output (round to nearest
+ * even). The caches must already hold the prefix and (after cw_kv_append) the
+ * suffix. Block IDs outside [0, num_blocks) read as zeros (never fault).
+ *   plan_dev    device copy of a plan from cw_suffix_prefill_plan for the same
+ *               cu_suffix / prefix_len / heads / head_dim
+ *   num_tiles   its out_num_tiles
+ * CW_EINVAL: NULL pointer, batch < 1, Hq % Hkv != 0, P_r % bs != 0, cu not
+ * non-decreasing from 0, ceil(L_r / bs) > bt_stride, num_tiles not matching the
+ * shape, softmax_scale not finite and positive.
+ * CW_EUNSUPPORTED: head_dim not 64/128, block_size != 16, Hq / Hkv > 128.
+ * CW_EHIP: launch failure. */
+cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void* v_cache,
+                                 const int32_t* block_table, int32_t bt_stride,
+                                 const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
+                                 const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                 int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                 int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                                 float softmax_scale, const int32_t* plan_dev, int32_t num_tiles,
+                                 void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CW_H */

@@ -32,6 +32,36 @@ def _as_f64(x) -> np.ndarray:
     return np.asarray(x, dtype=np.float64)
 
 
+def _attend_rows(q_rows: np.ndarray, k: np.ndarray, v: np.ndarray, row_pos: np.ndarray,
+                 scale: float) -> np.ndarray:
+    """Rows of attention: query rows q_rows [R, Hq, D] at absolute positions
+    row_pos [R] over keys/values k, v [L, Hkv, D]; row n sees keys 0 .. row_pos[n]."""
+    R, Hq, D = q_rows.shape
+    L, Hkv, _ = k.shape
+    G = Hq // Hkv
+    out = np.zeros((R, Hq, D), dtype=np.float64)
+    visible = np.arange(L)[None, :] <= row_pos[:, None]           # [R, L]
+    for g in range(Hkv):
+        qg = q_rows[:, g * G:(g + 1) * G, :]                         # [R, G, D]
+        scores = scale * (qg @ k[:, g, :].T)                         # [R, G, L]
+        scores = np.where(visible[:, None, :], scores, -np.inf)
+        m = scores.max(axis=2, keepdims=True)
+        w = np.exp(scores - m)                                       # exp(-inf) = 0
+        out[:, g * G:(g + 1) * G, :] = (w @ v[:, g, :]) / w.sum(axis=2, keepdims=True)
+    return out
+
+
+def _check_shapes(q, k, v, prefix_len):
+    S, Hq, D = q.shape
+    L, Hkv, Dk = k.shape
+    if Dk != D or v.shape != k.shape:
+        raise ValueError("k/v shape mismatch")
+    if L != prefix_len + S:
+        raise ValueError(f"logical length {L} != prefix {prefix_len} + suffix {S}")
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+
+
 def suffix_prefill_attention(q, k, v, prefix_len: int, scale: float,
                              row_chunk: int = 256) -> np.ndarray:
     """Attention output of the S suffix rows of one request.
@@ -48,32 +78,12 @@ def suffix_prefill_attention(q, k, v, prefix_len: int, scale: float,
     q = _as_f64(q)
     k = _as_f64(k)
     v = _as_f64(v)
-    S, Hq, D = q.shape
-    L, Hkv, Dk = k.shape
-    if Dk != D or v.shape != k.shape:
-        raise ValueError("k/v shape mismatch")
-    if L != prefix_len + S:
-        raise ValueError(f"logical length {L} != prefix {prefix_len} + suffix {S}")
-    if Hq % Hkv:
-        raise ValueError("Hq must be a multiple of Hkv")
-    G = Hq // Hkv
-    out = np.zeros((S, Hq, D), dtype=np.float64)
-    if S == 0:
-        return out
-    key_pos = np.arange(L)
-    for g in range(Hkv):
-        kg = k[:, g, :]                      # [L, D]
-        vg = v[:, g, :]                      # [L, D]
-        for r0 in range(0, S, row_chunk):
-            r1 = min(S, r0 + row_chunk)
-            qg = q[r0:r1, g * G:(g + 1) * G, :]          # [R, G, D]
-            scores = scale * (qg @ kg.T)                   # [R, G, L]
-            row_pos = prefix_len + np.arange(r0, r1)       # absolute positions
-            visible = key_pos[None, :] <= row_pos[:, None]  # [R, L]
-            scores = np.where(visible[:, None, :], scores, -np.inf)
-            m = scores.max(axis=2, keepdims=True)
-            w = np.exp(scores - m)                         # exp(-inf) = 0
-            out[r0:r1, g * G:(g + 1) * G, :] = (w @ vg) / w.sum(axis=2, keepdims=True)
+    _check_shapes(q, k, v, prefix_len)
+    S = q.shape[0]
+    out = np.zeros(q.shape, dtype=np.float64)
+    for r0 in range(0, S, row_chunk):
+        r1 = min(S, r0 + row_chunk)
+        out[r0:r1] = _attend_rows(q[r0:r1], k, v, prefix_len + np.arange(r0, r1), scale)
     return out
 
 
@@ -113,21 +123,24 @@ def batch_suffix_prefill_attention(qs, ks, vs, prefix_lens, scale: float) -> lis
             for q, k, v, p in zip(qs, ks, vs, prefix_lens)]
 
 
-def suffix_prefill_rows(q, k, v, prefix_len: int, scale: float, rows) -> np.ndarray:
+def suffix_prefill_rows(q, k, v, prefix_len: int, scale: float, rows,
+                        row_chunk: int = 256) -> np.ndarray:
     """Output of selected suffix rows only: [len(rows), Hq, D] float64.
 
     Each row depends only on its own query and keys 0 .. prefix_len + row, so a
-    sampled row is computed exactly as in the full call.
+    sampled row is computed exactly as in the full call. q holds all S rows.
     """
     q = _as_f64(q)
+    k = _as_f64(k)
+    v = _as_f64(v)
     rows = np.asarray(rows, dtype=np.int64)
-    res = np.zeros((len(rows), q.shape[1], q.shape[2]), dtype=np.float64)
-    kf = _as_f64(k)
-    vf = _as_f64(v)
-    for n, i in enumerate(rows):
-        L = prefix_len + int(i) + 1
-        res[n] = suffix_prefill_attention(q[i:i + 1], kf[:L], vf[:L], prefix_len + int(i), scale)[0]
-    return res
+    _check_shapes(q, k, v, prefix_len)
+    q_sel = q[rows]
+    out = np.zeros((len(rows),) + q.shape[1:], dtype=np.float64)
+    for r0 in range(0, len(rows), row_chunk):
+        r1 = min(len(rows), r0 + row_chunk)
+        out[r0:r1] = _attend_rows(q_sel[r0:r1], k, v, prefix_len + rows[r0:r1], scale)
+    return out
 
 
 def attention_flops(prefix_lens, suffix_lens, num_q_heads: int, head_dim: int) -> int:

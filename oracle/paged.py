@@ -115,8 +115,9 @@ class PoolSim:
     * alloc: hands out blocks from the front of the free queue; a block handed
       out forgets its stored hash (that is eviction). Too few free blocks: no
       change, error.
-    * commit: stores hash -> block for owned blocks; if the hash is already
-      stored for another block the map keeps the first one.
+    * commit: stores hash -> block for held blocks (a block may store one hash
+      only, and may not be listed with two); if the hash is already stored for
+      another block the map keeps the first one.
     * release: drops one reference per listed block; blocks reaching zero join
       the back of the free queue in reverse listing order, so the tail of a
       released sequence is reused before its head.
@@ -161,11 +162,14 @@ class PoolSim:
     def commit(self, hashes, ids):
         hashes = [int(h) for h in hashes]
         ids = [int(b) for b in ids]
+        pending = {}
         for h, b in zip(hashes, ids):
             if not (0 <= b < self.num_blocks) or self.ref[b] == 0:
                 raise ValueError("commit of a block that is not held")
             if self.hash_of[b] is not None and self.hash_of[b] != h:
                 raise ValueError("block already holds another hash")
+            if pending.setdefault(b, h) != h:
+                raise ValueError("block listed with two hashes")
         for h, b in zip(hashes, ids):
             if self.hash_of[b] is not None:
                 continue

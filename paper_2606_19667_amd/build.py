@@ -1,0 +1,71 @@
+"""Builds libcw.so in-tree for gfx950.
+
+    python -m paper_2606_19667_amd.build
+
+The host sources build with g++, the HIP sources with hipcc for gfx950; hipcc
+links the shared library against the HIP runtime.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG, "libcw.so")
+
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+HIPCC = os.path.join(ROCM, "bin", "hipcc")
+ARCH = "gfx950"
+
+HOST_SOURCES = ["cw_host.cpp"]
+HIP_SOURCES = ["cw_kernels.hip"]
+
+HIP_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    "-mcode-object-version=5",
+    # keep the compiler from forming packed fp32 VALU instructions
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-command-line-argument",
+]
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra"]
+
+
+def _run(cmd):
+    proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if proc.returncode != 0:
+        raise RuntimeError("build step failed:\n" + " ".join(cmd) + "\n" + proc.stdout)
+    return proc.stdout
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles every source and links libcw.so; returns its path."""
+    incs = [f"-I{INCLUDE}", f"-I{CSRC}"]
+    with tempfile.TemporaryDirectory(prefix="cw_build_") as tmp:
+        objs = []
+        for src in HOST_SOURCES:
+            obj = os.path.join(tmp, src + ".o")
+            out = _run([shutil.which("g++") or "g++", *HOST_FLAGS, *incs, "-c",
+                        os.path.join(CSRC, src), "-o", obj])
+            objs.append(obj)
+            if verbose and out:
+                print(out)
+        for src in HIP_SOURCES:
+            obj = os.path.join(tmp, src + ".o")
+            out = _run([HIPCC, *HIP_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
+            objs.append(obj)
+            if verbose and out:
+                print(out)
+        tmp_lib = os.path.join(tmp, "libcw.so")
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp_lib])
+        shutil.move(tmp_lib, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

@@ -1,0 +1,721 @@
+// Host half of libcw: status reporting, chained block hashes, the block pool
+// with prefix lookup, batch scheduling, and the attention tile planner.
+//
+// Paper Sec. 2.1 (with Fig. 1): KV memory lives in fixed-size token blocks;
+// each block is hashed together with its prefix history and a new prompt
+// reuses the longest leading run of stored blocks. Sec. 3.4: residency and
+// eviction belong to the engine. The hash function is not named in the paper;
+// this library uses XXH64 keyed by the previous block's hash.
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "cw_internal.h"
+
+static_assert(__BYTE_ORDER__ == __ORDER_LITTLE_ENDIAN__, "token bytes are hashed in host order");
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+namespace cw {
+
+cw_status fail(cw_status status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+cw_status ok() {
+  g_last_error.clear();
+  return CW_OK;
+}
+
+cw_status check_batch(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t block_size,
+                      int32_t bt_stride, int64_t* total_rows) {
+  if (batch < 1) return fail(CW_EINVAL, "batch must be >= 1");
+  if (!cu || !plen) return fail(CW_EINVAL, "cu_suffix_host and prefix_len_host are required");
+  if (block_size < 1) return fail(CW_EINVAL, "block_size must be >= 1");
+  if (bt_stride < 1) return fail(CW_EINVAL, "bt_stride must be >= 1");
+  if (cu[0] != 0) return fail(CW_EINVAL, "cu_suffix[0] must be 0");
+  for (int32_t r = 0; r < batch; ++r) {
+    if (cu[r + 1] < cu[r]) return fail(CW_EINVAL, "cu_suffix must be non-decreasing");
+    if (plen[r] < 0 || plen[r] % block_size != 0)
+      return fail(CW_EINVAL, "prefix_len[" + std::to_string(r) + "] = " + std::to_string(plen[r]) +
+                                 " is not a non-negative multiple of the block size");
+    const int64_t L = int64_t(plen[r]) + (cu[r + 1] - cu[r]);
+    const int64_t nb = (L + block_size - 1) / block_size;
+    if (nb > bt_stride)
+      return fail(CW_EINVAL, "request " + std::to_string(r) + " needs " + std::to_string(nb) +
+                                 " blocks but bt_stride is " + std::to_string(bt_stride));
+  }
+  if (total_rows) *total_rows = cu[batch];
+  return CW_OK;
+}
+
+int64_t count_tiles(const int32_t* cu, int32_t batch, int32_t hkv, int32_t per_tile) {
+  int64_t n = 0;
+  for (int32_t r = 0; r < batch; ++r) n += (int64_t(cu[r + 1] - cu[r]) + per_tile - 1) / per_tile;
+  return n * hkv;
+}
+
+}  // namespace cw
+
+using cw::fail;
+
+extern "C" int32_t cw_abi_version(void) { return CW_ABI_VERSION; }
+
+extern "C" const char* cw_last_error(void) { return g_last_error.c_str(); }
+
+// ---------------------------------------------------------------------------
+// XXH64 (the published xxHash 64-bit algorithm: four accumulator lanes over
+// 32-byte stripes, 8/4/1-byte tails, final avalanche).
+// ---------------------------------------------------------------------------
+namespace {
+constexpr uint64_t kP1 = 0x9E3779B185EBCA87ULL;
+constexpr uint64_t kP2 = 0xC2B2AE3D27D4EB4FULL;
+constexpr uint64_t kP3 = 0x165667B19E3779F9ULL;
+constexpr uint64_t kP4 = 0x85EBCA77C2B2AE63ULL;
+constexpr uint64_t kP5 = 0x27D4EB2F165667C5ULL;
+
+inline uint64_t rotl64(uint64_t x, int r) { return (x << r) | (x >> (64 - r)); }
+inline uint64_t rd64(const uint8_t* p) { uint64_t v; std::memcpy(&v, p, 8); return v; }
+inline uint32_t rd32(const uint8_t* p) { uint32_t v; std::memcpy(&v, p, 4); return v; }
+inline uint64_t xround(uint64_t acc, uint64_t lane) { return rotl64(acc + lane * kP2, 31) * kP1; }
+inline uint64_t xmerge(uint64_t acc, uint64_t v) { return (acc ^ xround(0, v)) * kP1 + kP4; }
+
+uint64_t xxh64(const uint8_t* p, size_t n, uint64_t seed) {
+  const uint8_t* end = p + n;
+  uint64_t acc;
+  if (n >= 32) {
+    uint64_t v1 = seed + kP1 + kP2, v2 = seed + kP2, v3 = seed, v4 = seed - kP1;
+    for (; p + 32 <= end; p += 32) {
+      v1 = xround(v1, rd64(p));
+      v2 = xround(v2, rd64(p + 8));
+      v3 = xround(v3, rd64(p + 16));
+      v4 = xround(v4, rd64(p + 24));
+    }
+    acc = rotl64(v1, 1) + rotl64(v2, 7) + rotl64(v3, 12) + rotl64(v4, 18);
+    acc = xmerge(acc, v1);
+    acc = xmerge(acc, v2);
+    acc = xmerge(acc, v3);
+    acc = xmerge(acc, v4);
+  } else {
+    acc = seed + kP5;
+  }
+  acc += n;
+  for (; p + 8 <= end; p += 8) acc = rotl64(acc ^ xround(0, rd64(p)), 27) * kP1 + kP4;
+  if (p + 4 <= end) {
+    acc = rotl64(acc ^ (uint64_t(rd32(p)) * kP1), 23) * kP2 + kP3;
+    p += 4;
+  }
+  for (; p < end; ++p) acc = rotl64(acc ^ (uint64_t(*p) * kP5), 11) * kP1;
+  acc ^= acc >> 33;
+  acc *= kP2;
+  acc ^= acc >> 29;
+  acc *= kP3;
+  acc ^= acc >> 32;
+  return acc;
+}
+
+void chain_hashes(const int32_t* tokens, int64_t n_tokens, int32_t bs, uint64_t* out) {
+  uint64_t h = 0;
+  const int64_t nb = n_tokens / bs;
+  for (int64_t b = 0; b < nb; ++b) {
+    h = xxh64(reinterpret_cast<const uint8_t*>(tokens + b * bs), size_t(bs) * 4, h);
+    out[b] = h;
+  }
+}
+}  // namespace
+
+extern "C" cw_status cw_block_hashes(const int32_t* tokens, int64_t n_tokens, int32_t block_size,
+                                     uint64_t* out_hashes) {
+  if (n_tokens < 0) return fail(CW_EINVAL, "n_tokens must be >= 0");
+  if (block_size < 1) return fail(CW_EINVAL, "block_size must be >= 1");
+  if (n_tokens / block_size > 0 && (!tokens || !out_hashes))
+    return fail(CW_EINVAL, "tokens and out_hashes are required");
+  chain_hashes(tokens, n_tokens, block_size, out_hashes);
+  return cw::ok();
+}
+
+// ---------------------------------------------------------------------------
+// Block pool. The free queue is a doubly linked list threaded through
+// prev/next (index n is the sentinel). Unlinking leaves a node's own links in
+// place, so an undo log replayed in reverse can relink nodes exactly. Stored
+// hashes live in a flat open-addressing index, so a pool is a handful of
+// arrays and cloning one is a few memory copies.
+// ---------------------------------------------------------------------------
+namespace {
+
+// Map from stored block hash to block ID: linear probing, backward-shift
+// deletion, capacity a power of two >= 2 * num_blocks (each block stores at
+// most one hash, so the load factor stays <= 1/2).
+struct HashIndex {
+  std::vector<uint64_t> key;
+  std::vector<int32_t> val;  // -1 marks an empty slot
+  uint64_t mask = 0;
+  int shift = 64;
+
+  void init(int32_t nblocks) {
+    size_t cap = 16;
+    int lg = 4;
+    while (cap < 2 * size_t(nblocks)) {
+      cap <<= 1;
+      ++lg;
+    }
+    key.assign(cap, 0);
+    val.assign(cap, -1);
+    mask = cap - 1;
+    shift = 64 - lg;
+  }
+  size_t home(uint64_t k) const { return size_t((k * 0x9E3779B97F4A7C15ULL) >> shift); }
+  int32_t find(uint64_t k) const {
+    for (size_t i = home(k);; i = (i + 1) & mask) {
+      if (val[i] < 0) return -1;
+      if (key[i] == k) return val[i];
+    }
+  }
+  // Caller guarantees k is absent.
+  void insert(uint64_t k, int32_t v) {
+    size_t i = home(k);
+    while (val[i] >= 0) i = (i + 1) & mask;
+    key[i] = k;
+    val[i] = v;
+  }
+  void erase(uint64_t k) {
+    size_t i = home(k);
+    while (true) {
+      if (val[i] < 0) return;
+      if (key[i] == k) break;
+      i = (i + 1) & mask;
+    }
+    size_t j = i;
+    while (true) {
+      j = (j + 1) & mask;
+      if (val[j] < 0) break;
+      const size_t h = home(key[j]);
+      if (((j - h) & mask) >= ((j - i) & mask)) {  // entry j may move back into the hole
+        key[i] = key[j];
+        val[i] = val[j];
+        i = j;
+      }
+    }
+    val[i] = -1;
+  }
+};
+
+}  // namespace
+
+struct cw_pool {
+  int32_t n = 0;
+  std::vector<int32_t> ref;
+  std::vector<uint64_t> hash;
+  std::vector<uint8_t> has_hash;
+  std::vector<int32_t> prev, next;
+  int32_t nfree = 0;
+  HashIndex table;
+
+  void unlink(int32_t b) {
+    next[prev[b]] = next[b];
+    prev[next[b]] = prev[b];
+    --nfree;
+  }
+  void relink(int32_t b) {  // inverse of the most recent unlink(b)
+    next[prev[b]] = b;
+    prev[next[b]] = b;
+    ++nfree;
+  }
+  void push_back(int32_t b) {
+    const int32_t s = n;
+    prev[b] = prev[s];
+    next[b] = s;
+    next[prev[s]] = b;
+    prev[s] = b;
+    ++nfree;
+  }
+  int32_t front() const { return next[n]; }
+};
+
+namespace {
+
+// Mutations made by a multi-step call, undone in reverse on failure.
+struct UndoLog {
+  enum Kind : uint8_t { kAcquireFree, kAcquireHeld, kAlloc, kCommit };
+  struct Entry {
+    Kind kind;
+    uint8_t had_hash;
+    int32_t block;
+    uint64_t hash;
+  };
+  std::vector<Entry> entries;
+
+  void rollback(cw_pool* p) {
+    for (auto it = entries.rbegin(); it != entries.rend(); ++it) {
+      const int32_t b = it->block;
+      switch (it->kind) {
+        case kAcquireFree:
+          p->ref[b] = 0;
+          p->relink(b);
+          break;
+        case kAcquireHeld:
+          p->ref[b] -= 1;
+          break;
+        case kAlloc:
+          p->ref[b] = 0;
+          p->relink(b);
+          if (it->had_hash) {
+            p->has_hash[b] = 1;
+            p->hash[b] = it->hash;
+            p->table.insert(it->hash, b);
+          }
+          break;
+        case kCommit:
+          p->table.erase(it->hash);
+          p->has_hash[b] = 0;
+          break;
+      }
+    }
+    entries.clear();
+  }
+};
+
+void acquire(cw_pool* p, int32_t b, UndoLog* log) {
+  if (p->ref[b] == 0) {
+    p->unlink(b);
+    if (log) log->entries.push_back({UndoLog::kAcquireFree, 0, b, 0});
+  } else if (log) {
+    log->entries.push_back({UndoLog::kAcquireHeld, 0, b, 0});
+  }
+  p->ref[b] += 1;
+}
+
+int32_t match(cw_pool* p, const uint64_t* hashes, int32_t n, int32_t max_match, int32_t* out,
+              UndoLog* log) {
+  int32_t depth = 0;
+  const int32_t lim = std::min(n, std::max(0, max_match));
+  while (depth < lim) {
+    const int32_t b = p->table.find(hashes[depth]);
+    if (b < 0) break;
+    out[depth++] = b;
+  }
+  for (int32_t i = 0; i < depth; ++i) acquire(p, out[i], log);
+  return depth;
+}
+
+// Caller has checked nfree >= count.
+void alloc_n(cw_pool* p, int32_t count, int32_t* out, UndoLog* log) {
+  for (int32_t i = 0; i < count; ++i) {
+    const int32_t b = p->front();
+    p->unlink(b);
+    const uint8_t had = p->has_hash[b];
+    const uint64_t old = p->hash[b];
+    if (had) {
+      p->table.erase(old);
+      p->has_hash[b] = 0;
+    }
+    p->ref[b] = 1;
+    if (log) log->entries.push_back({UndoLog::kAlloc, had, b, old});
+    out[i] = b;
+  }
+}
+
+// Caller has validated the (hash, block) pairs.
+void commit_n(cw_pool* p, const uint64_t* hashes, const int32_t* ids, int32_t n, UndoLog* log) {
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t b = ids[i];
+    if (p->has_hash[b]) continue;
+    if (p->table.find(hashes[i]) >= 0) continue;
+    p->table.insert(hashes[i], b);
+    p->has_hash[b] = 1;
+    p->hash[b] = hashes[i];
+    if (log) log->entries.push_back({UndoLog::kCommit, 0, b, hashes[i]});
+  }
+}
+
+// Per-thread scratch indexed by block ID for validating one call's arguments.
+struct Scratch {
+  std::vector<int32_t> count;
+  std::vector<uint64_t> hash;
+  std::vector<int32_t> touched;
+  void fit(int32_t n) {
+    if (int32_t(count.size()) < n) {
+      count.resize(size_t(n), 0);
+      hash.resize(size_t(n), 0);
+    }
+    touched.clear();
+  }
+  void reset() {
+    for (int32_t b : touched) count[size_t(b)] = 0;
+    touched.clear();
+  }
+};
+thread_local Scratch g_scratch;
+
+cw_status check_commit(const cw_pool* p, const uint64_t* hashes, const int32_t* ids, int32_t n) {
+  Scratch& sc = g_scratch;
+  sc.fit(p->n);
+  cw_status st = CW_OK;
+  for (int32_t i = 0; i < n && st == CW_OK; ++i) {
+    const int32_t b = ids[i];
+    if (b < 0 || b >= p->n) {
+      st = fail(CW_EINVAL, "commit: block ID out of range");
+    } else if (p->ref[b] == 0) {
+      st = fail(CW_EINVAL, "commit: block " + std::to_string(b) + " is not held");
+    } else if (p->has_hash[b] && p->hash[b] != hashes[i]) {
+      st = fail(CW_EINVAL, "commit: block " + std::to_string(b) + " already holds another hash");
+    } else if (sc.count[size_t(b)] && sc.hash[size_t(b)] != hashes[i]) {
+      st = fail(CW_EINVAL, "commit: block " + std::to_string(b) + " listed with two hashes");
+    } else if (!sc.count[size_t(b)]) {
+      sc.count[size_t(b)] = 1;
+      sc.hash[size_t(b)] = hashes[i];
+      sc.touched.push_back(b);
+    }
+  }
+  sc.reset();
+  return st;
+}
+
+cw_status check_release(const cw_pool* p, const int32_t* ids, int32_t n) {
+  Scratch& sc = g_scratch;
+  sc.fit(p->n);
+  cw_status st = CW_OK;
+  for (int32_t i = 0; i < n && st == CW_OK; ++i) {
+    const int32_t b = ids[i];
+    if (b < 0 || b >= p->n) {
+      st = fail(CW_EINVAL, "release: block ID out of range");
+    } else {
+      if (sc.count[size_t(b)]++ == 0) sc.touched.push_back(b);
+      if (sc.count[size_t(b)] > p->ref[b])
+        st = fail(CW_EINVAL, "release: block " + std::to_string(b) + " is not held that often");
+    }
+  }
+  sc.reset();
+  return st;
+}
+
+void release_n(cw_pool* p, const int32_t* ids, int32_t n) {
+  for (int32_t i = n - 1; i >= 0; --i) {
+    const int32_t b = ids[i];
+    if (--p->ref[b] == 0) p->push_back(b);
+  }
+}
+
+}  // namespace
+
+extern "C" cw_status cw_pool_create(int32_t num_blocks, const int32_t* free_order, cw_pool** out) {
+  if (!out) return fail(CW_EINVAL, "out is required");
+  *out = nullptr;
+  if (num_blocks < 1) return fail(CW_EINVAL, "num_blocks must be >= 1");
+  std::vector<int32_t> order(num_blocks);
+  if (free_order) {
+    std::vector<uint8_t> seen(num_blocks, 0);
+    for (int32_t i = 0; i < num_blocks; ++i) {
+      const int32_t b = free_order[i];
+      if (b < 0 || b >= num_blocks || seen[b]) return fail(CW_EINVAL, "free_order is not a permutation");
+      seen[b] = 1;
+      order[i] = b;
+    }
+  } else {
+    std::iota(order.begin(), order.end(), 0);
+  }
+  auto* p = new cw_pool();
+  p->n = num_blocks;
+  p->ref.assign(num_blocks, 0);
+  p->hash.assign(num_blocks, 0);
+  p->has_hash.assign(num_blocks, 0);
+  p->prev.assign(num_blocks + 1, num_blocks);
+  p->next.assign(num_blocks + 1, num_blocks);
+  p->table.init(num_blocks);
+  for (int32_t b : order) p->push_back(b);
+  *out = p;
+  return cw::ok();
+}
+
+extern "C" void cw_pool_destroy(cw_pool* pool) { delete pool; }
+
+extern "C" cw_status cw_pool_clone(const cw_pool* pool, cw_pool** out) {
+  if (!pool || !out) return fail(CW_EINVAL, "pool and out are required");
+  *out = new cw_pool(*pool);
+  return cw::ok();
+}
+
+extern "C" int32_t cw_pool_num_free(const cw_pool* pool) { return pool ? pool->nfree : -1; }
+
+extern "C" cw_status cw_prefix_match(cw_pool* pool, const uint64_t* hashes, int32_t n_hashes,
+                                     int32_t max_match, int32_t* out_block_ids, int32_t* out_depth) {
+  if (!pool || !out_depth) return fail(CW_EINVAL, "pool and out_depth are required");
+  if (n_hashes < 0) return fail(CW_EINVAL, "n_hashes must be >= 0");
+  if (n_hashes > 0 && (!hashes || !out_block_ids))
+    return fail(CW_EINVAL, "hashes and out_block_ids are required");
+  *out_depth = match(pool, hashes, n_hashes, max_match, out_block_ids, nullptr);
+  return cw::ok();
+}
+
+extern "C" cw_status cw_pool_alloc(cw_pool* pool, int32_t n, int32_t* out_block_ids) {
+  if (!pool) return fail(CW_EINVAL, "pool is required");
+  if (n < 0) return fail(CW_EINVAL, "n must be >= 0");
+  if (n > 0 && !out_block_ids) return fail(CW_EINVAL, "out_block_ids is required");
+  if (n > pool->nfree)
+    return fail(CW_ENOSPC, "pool exhausted: " + std::to_string(n) + " blocks requested, " +
+                               std::to_string(pool->nfree) + " free");
+  alloc_n(pool, n, out_block_ids, nullptr);
+  return cw::ok();
+}
+
+extern "C" cw_status cw_pool_commit(cw_pool* pool, const uint64_t* hashes, const int32_t* block_ids,
+                                    int32_t n) {
+  if (!pool) return fail(CW_EINVAL, "pool is required");
+  if (n < 0) return fail(CW_EINVAL, "n must be >= 0");
+  if (n > 0 && (!hashes || !block_ids)) return fail(CW_EINVAL, "hashes and block_ids are required");
+  cw_status st = check_commit(pool, hashes, block_ids, n);
+  if (st != CW_OK) return st;
+  commit_n(pool, hashes, block_ids, n, nullptr);
+  return cw::ok();
+}
+
+extern "C" cw_status cw_pool_release(cw_pool* pool, const int32_t* block_ids, int32_t n) {
+  if (!pool) return fail(CW_EINVAL, "pool is required");
+  if (n < 0) return fail(CW_EINVAL, "n must be >= 0");
+  if (n > 0 && !block_ids) return fail(CW_EINVAL, "block_ids is required");
+  cw_status st = check_release(pool, block_ids, n);
+  if (st != CW_OK) return st;
+  release_n(pool, block_ids, n);
+  return cw::ok();
+}
+
+extern "C" cw_status cw_schedule_batch(cw_pool* pool, const int32_t* tokens, const int64_t* cu_tokens,
+                                       int32_t batch, int32_t block_size, int32_t bt_stride,
+                                       int32_t* out_block_table, int32_t* out_prefix_len,
+                                       int32_t* out_cu_suffix) {
+  if (!pool || !tokens || !cu_tokens || !out_block_table || !out_prefix_len || !out_cu_suffix)
+    return fail(CW_EINVAL, "a required pointer is NULL");
+  if (batch < 1) return fail(CW_EINVAL, "batch must be >= 1");
+  if (block_size < 1 || bt_stride < 1) return fail(CW_EINVAL, "block_size and bt_stride must be >= 1");
+  if (cu_tokens[0] != 0) return fail(CW_EINVAL, "cu_tokens[0] must be 0");
+  int64_t total_suffix = 0;
+  for (int32_t r = 0; r < batch; ++r) {
+    const int64_t L = cu_tokens[r + 1] - cu_tokens[r];
+    if (L < 1) return fail(CW_EINVAL, "request " + std::to_string(r) + " has an empty prompt");
+    if ((L + block_size - 1) / block_size > bt_stride)
+      return fail(CW_EINVAL, "request " + std::to_string(r) + " does not fit bt_stride");
+  }
+  UndoLog log;
+  std::vector<uint64_t> hashes;
+  out_cu_suffix[0] = 0;
+  for (int32_t r = 0; r < batch; ++r) {
+    const int64_t L = cu_tokens[r + 1] - cu_tokens[r];
+    const int64_t nfull = L / block_size;
+    const int64_t nblocks = (L + block_size - 1) / block_size;
+    hashes.resize(size_t(nfull));
+    chain_hashes(tokens + cu_tokens[r], L, block_size, hashes.data());
+    int32_t* row = out_block_table + int64_t(r) * bt_stride;
+    const int32_t cap = int32_t((L - 1) / block_size);
+    const int32_t depth = match(pool, hashes.data(), int32_t(nfull), cap, row, &log);
+    const int32_t fresh = int32_t(nblocks - depth);
+    if (fresh > pool->nfree) {
+      log.rollback(pool);
+      return fail(CW_ENOSPC, "pool exhausted while scheduling request " + std::to_string(r));
+    }
+    alloc_n(pool, fresh, row + depth, &log);
+    commit_n(pool, hashes.data() + depth, row + depth, int32_t(nfull - depth), &log);
+    for (int64_t i = nblocks; i < bt_stride; ++i) row[i] = -1;
+    out_prefix_len[r] = depth * block_size;
+    total_suffix += L - int64_t(depth) * block_size;
+    if (total_suffix > INT32_MAX) {
+      log.rollback(pool);
+      return fail(CW_EINVAL, "total suffix rows exceed INT32_MAX");
+    }
+    out_cu_suffix[r + 1] = int32_t(total_suffix);
+  }
+  return cw::ok();
+}
+
+extern "C" cw_status cw_release_batch(cw_pool* pool, const int32_t* block_table, int32_t bt_stride,
+                                      const int32_t* prefix_len, const int32_t* cu_suffix,
+                                      int32_t batch, int32_t block_size) {
+  if (!pool || !block_table) return fail(CW_EINVAL, "pool and block_table are required");
+  cw_status st = cw::check_batch(cu_suffix, prefix_len, batch, block_size, bt_stride, nullptr);
+  if (st != CW_OK) return st;
+  std::vector<int32_t> ids;
+  for (int32_t r = 0; r < batch; ++r) {
+    const int64_t L = int64_t(prefix_len[r]) + (cu_suffix[r + 1] - cu_suffix[r]);
+    const int64_t nb = (L + block_size - 1) / block_size;
+    ids.insert(ids.end(), block_table + int64_t(r) * bt_stride, block_table + int64_t(r) * bt_stride + nb);
+  }
+  st = check_release(pool, ids.data(), int32_t(ids.size()));
+  if (st != CW_OK) return st;
+  // Per request, so each request's tail is reused before its head.
+  size_t off = 0;
+  for (int32_t r = 0; r < batch; ++r) {
+    const int64_t L = int64_t(prefix_len[r]) + (cu_suffix[r + 1] - cu_suffix[r]);
+    const int32_t nb = int32_t((L + block_size - 1) / block_size);
+    release_n(pool, ids.data() + off, nb);
+    off += nb;
+  }
+  return cw::ok();
+}
+
+// ---------------------------------------------------------------------------
+// Tile planner. A tile is (request, KV head, first suffix row); its cost is the
+// number of KV tiles its rows visit under the causal limit. Tiles are listed
+// heaviest first; when there are enough (request, KV head) pairs, each pair is
+// pinned to one L2 partition (pairs balanced by total cost) so the tiles that
+// re-read a pair's K/V share that partition's L2, and the per-partition queues
+// are interleaved so that workgroup i lands on partition i % 8. Empty entries
+// (request -1) pad the shorter queues.
+// ---------------------------------------------------------------------------
+namespace {
+
+cw_status plan_args(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv,
+                    int32_t d) {
+  if (!cu || !plen) return fail(CW_EINVAL, "cu_suffix_host and prefix_len_host are required");
+  if (batch < 1) return fail(CW_EINVAL, "batch must be >= 1");
+  if (hq < 1 || hkv < 1 || hq % hkv != 0)
+    return fail(CW_EINVAL, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (hq / hkv > cw::kTileRows) return fail(CW_EUNSUPPORTED, "more than 128 query heads per KV head");
+  if (d != 64 && d != 128) return fail(CW_EUNSUPPORTED, "head_dim must be 64 or 128");
+  if (cu[0] != 0) return fail(CW_EINVAL, "cu_suffix[0] must be 0");
+  for (int32_t r = 0; r < batch; ++r) {
+    if (cu[r + 1] < cu[r]) return fail(CW_EINVAL, "cu_suffix must be non-decreasing");
+    if (plen[r] < 0) return fail(CW_EINVAL, "prefix_len must be >= 0");
+  }
+  return CW_OK;
+}
+
+inline int32_t tile_cost(int32_t P, int32_t row0, int32_t S, int32_t per) {
+  const int64_t kv_end = int64_t(P) + row0 + std::min(per, S - row0);
+  return int32_t((kv_end + cw::kKvTile - 1) / cw::kKvTile);
+}
+
+// Which partition queue each (request, KV head) pair feeds (-1: one plain
+// queue) and the padded plan length.
+struct PlanShape {
+  int32_t per = 0;
+  int64_t tiles = 0;
+  int64_t padded = 0;
+  int32_t max_cost = 0;
+  std::vector<int8_t> part;  // [batch * hkv], empty when not grouped
+};
+
+PlanShape plan_shape(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv) {
+  PlanShape ps;
+  ps.per = cw::tile_positions(hq / hkv);
+  std::vector<int64_t> req_cost(size_t(batch), 0), req_count(size_t(batch), 0);
+  int64_t total = 0;
+  for (int32_t r = 0; r < batch; ++r) {
+    const int32_t S = cu[r + 1] - cu[r];
+    for (int32_t row0 = 0; row0 < S; row0 += ps.per) {
+      const int32_t c = tile_cost(plen[r], row0, S, ps.per);
+      req_cost[size_t(r)] += c;
+      req_count[size_t(r)] += 1;
+      ps.max_cost = std::max(ps.max_cost, c);
+    }
+    ps.tiles += req_count[size_t(r)] * hkv;
+    total += req_cost[size_t(r)] * hkv;
+  }
+  ps.padded = ps.tiles;
+  const int64_t npairs = int64_t(batch) * hkv;
+  if (npairs < 4 * cw::kNumXcd) return ps;
+  std::vector<int32_t> order(static_cast<size_t>(batch));
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int32_t a, int32_t b) { return req_cost[size_t(a)] > req_cost[size_t(b)]; });
+  std::vector<int8_t> part(size_t(npairs), 0);
+  int64_t load[cw::kNumXcd] = {0};
+  int64_t len[cw::kNumXcd] = {0};
+  for (int32_t r : order)
+    for (int32_t g = 0; g < hkv; ++g) {
+      int x = 0;
+      for (int i = 1; i < cw::kNumXcd; ++i)
+        if (load[i] < load[x]) x = i;
+      part[size_t(int64_t(r) * hkv + g)] = int8_t(x);
+      load[x] += req_cost[size_t(r)];
+      len[x] += req_count[size_t(r)];
+    }
+  const int64_t max_load = *std::max_element(load, load + cw::kNumXcd);
+  if (max_load * cw::kNumXcd > total + total / 20) return ps;  // >5% imbalance: one plain queue
+  ps.part = std::move(part);
+  ps.padded = *std::max_element(len, len + cw::kNumXcd) * cw::kNumXcd;
+  return ps;
+}
+
+// Writes the plan: 4 int32 per entry {request, kv head, first row, cost}.
+void write_plan(const PlanShape& ps, const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hkv,
+                int32_t* out) {
+  const int nq = ps.part.empty() ? 1 : cw::kNumXcd;
+  const int32_t nc = ps.max_cost + 1;
+  // Counting sort by (queue, cost descending); ties keep generation order
+  // (request, first row, KV head).
+  std::vector<int64_t> start(size_t(nq) * nc, 0);
+  auto queue_of = [&](int32_t r, int32_t g) { return ps.part.empty() ? 0 : int(ps.part[size_t(int64_t(r) * hkv + g)]); };
+  for (int32_t r = 0; r < batch; ++r) {
+    const int32_t S = cu[r + 1] - cu[r];
+    for (int32_t row0 = 0; row0 < S; row0 += ps.per) {
+      const int32_t c = tile_cost(plen[r], row0, S, ps.per);
+      for (int32_t g = 0; g < hkv; ++g) start[size_t(queue_of(r, g)) * nc + (nc - 1 - c)] += 1;
+    }
+  }
+  std::vector<int64_t> qlen(size_t(nq), 0);
+  for (int x = 0; x < nq; ++x) {
+    int64_t acc = 0;
+    for (int32_t k = 0; k < nc; ++k) {
+      const int64_t n = start[size_t(x) * nc + k];
+      start[size_t(x) * nc + k] = acc;
+      acc += n;
+    }
+    qlen[size_t(x)] = acc;
+  }
+  // Queue x, position i  ->  plan entry i * nq + x. Pad first, then fill.
+  for (int64_t e = 0; e < ps.padded; ++e) {
+    out[4 * e + 0] = -1;
+    out[4 * e + 1] = 0;
+    out[4 * e + 2] = 0;
+    out[4 * e + 3] = 0;
+  }
+  for (int32_t r = 0; r < batch; ++r) {
+    const int32_t S = cu[r + 1] - cu[r];
+    for (int32_t row0 = 0; row0 < S; row0 += ps.per) {
+      const int32_t c = tile_cost(plen[r], row0, S, ps.per);
+      for (int32_t g = 0; g < hkv; ++g) {
+        const int x = queue_of(r, g);
+        const int64_t i = start[size_t(x) * nc + (nc - 1 - c)]++;
+        const int64_t e = i * nq + x;
+        out[4 * e + 0] = r;
+        out[4 * e + 1] = g;
+        out[4 * e + 2] = row0;
+        out[4 * e + 3] = c;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" int64_t cw_suffix_prefill_plan_words(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                                int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                                int32_t head_dim) {
+  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim);
+  if (st != CW_OK) return st;
+  const PlanShape ps = plan_shape(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads);
+  cw::ok();
+  return 4 * ps.padded;
+}
+
+extern "C" cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                            int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                            int32_t head_dim, int32_t* plan_host, int64_t plan_words,
+                                            int32_t* out_num_tiles) {
+  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim);
+  if (st != CW_OK) return st;
+  if (!out_num_tiles) return fail(CW_EINVAL, "out_num_tiles is required");
+  const PlanShape ps = plan_shape(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads);
+  if (ps.padded > INT32_MAX) return fail(CW_EUNSUPPORTED, "too many tiles");
+  if (4 * ps.padded > plan_words || (!plan_host && ps.padded > 0))
+    return fail(CW_EINVAL, "plan buffer too small: need " + std::to_string(4 * ps.padded) + " words");
+  write_plan(ps, cu_suffix_host, prefix_len_host, batch, num_kv_heads, plan_host);
+  *out_num_tiles = int32_t(ps.padded);
+  return cw::ok();
+}

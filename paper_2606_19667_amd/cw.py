@@ -1,0 +1,326 @@
+"""Python binding of libcw (include/cw.h): argument marshalling only.
+
+Every function here checks and converts its arguments, then calls the C entry
+point of the same name; all computation happens in the library (host C++ for
+hashing, the block pool and planning; HIP kernels on the GPU for the append and
+the attention). torch tensors provide device memory and the HIP stream.
+
+The library is loaded after torch so that both use the one HIP runtime that
+torch has already loaded. A missing library raises at import time: there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcw.so")
+
+CW_OK = 0
+CW_EINVAL = -1
+CW_EUNSUPPORTED = -2
+CW_ENOSPC = -3
+CW_EHIP = -4
+BLOCK_SIZE = 16
+
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_f32 = ctypes.c_float
+_vp = ctypes.c_void_p
+_pi32 = ctypes.POINTER(ctypes.c_int32)
+_pi64 = ctypes.POINTER(ctypes.c_int64)
+_pu64 = ctypes.POINTER(ctypes.c_uint64)
+
+
+class CwError(RuntimeError):
+    """A libcw call returned a non-OK status."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"libcw status {status}: {message}")
+        self.status = status
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_19667_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "cw_abi_version": (_i32, []),
+        "cw_last_error": (ctypes.c_char_p, []),
+        "cw_block_hashes": (_i32, [_pi32, _i64, _i32, _pu64]),
+        "cw_pool_create": (_i32, [_i32, _pi32, ctypes.POINTER(_vp)]),
+        "cw_pool_destroy": (None, [_vp]),
+        "cw_pool_clone": (_i32, [_vp, ctypes.POINTER(_vp)]),
+        "cw_pool_num_free": (_i32, [_vp]),
+        "cw_prefix_match": (_i32, [_vp, _pu64, _i32, _i32, _pi32, _pi32]),
+        "cw_pool_alloc": (_i32, [_vp, _i32, _pi32]),
+        "cw_pool_commit": (_i32, [_vp, _pu64, _pi32, _i32]),
+        "cw_pool_release": (_i32, [_vp, _pi32, _i32]),
+        "cw_schedule_batch": (_i32, [_vp, _pi32, _pi64, _i32, _i32, _i32, _pi32, _pi32, _pi32]),
+        "cw_release_batch": (_i32, [_vp, _pi32, _i32, _pi32, _pi32, _i32, _i32]),
+        "cw_kv_append": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
+                                _i32, _i32, _i32, _i32, _i32, _vp]),
+        "cw_suffix_prefill_plan_words": (_i64, [_pi32, _pi32, _i32, _i32, _i32, _i32]),
+        "cw_suffix_prefill_plan": (_i32, [_pi32, _pi32, _i32, _i32, _i32, _i32, _pi32, _i64, _pi32]),
+        "cw_suffix_prefill_attn": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
+                                          _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _i32,
+                                          _vp, _vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_create",
+            "cw_pool_destroy", "cw_pool_clone", "cw_pool_num_free", "cw_prefix_match",
+            "cw_pool_alloc", "cw_pool_commit", "cw_pool_release", "cw_schedule_batch",
+            "cw_release_batch", "cw_kv_append", "cw_suffix_prefill_plan_words",
+            "cw_suffix_prefill_plan", "cw_suffix_prefill_attn")
+
+
+def lib() -> ctypes.CDLL:
+    return _lib
+
+
+def abi_version() -> int:
+    return int(_lib.cw_abi_version())
+
+
+def last_error() -> str:
+    return _lib.cw_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != CW_OK:
+        raise CwError(int(status), last_error())
+
+
+def _i32_array(x, name: str) -> np.ndarray:
+    a = np.ascontiguousarray(np.asarray(x), dtype=np.int32)
+    return a
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype)) if a.size else None
+
+
+# ---------------------------------------------------------------- host calls
+def block_hashes(tokens, block_size: int = BLOCK_SIZE) -> np.ndarray:
+    """cw_block_hashes: chained hashes of the full blocks (uint64 array)."""
+    t = _i32_array(tokens, "tokens")
+    out = np.zeros(len(t) // block_size, dtype=np.uint64)
+    _check(_lib.cw_block_hashes(_ptr(t, ctypes.c_int32), len(t), block_size, _ptr(out, ctypes.c_uint64)))
+    return out
+
+
+class Pool:
+    """Owner of a cw_pool handle (host-side block bookkeeping)."""
+
+    def __init__(self, num_blocks: int | None = None, free_order=None, _handle=None):
+        if _handle is not None:
+            self._h = _handle
+            return
+        h = _vp()
+        fo = None if free_order is None else _i32_array(free_order, "free_order")
+        if fo is not None and len(fo) != num_blocks:
+            raise ValueError("free_order must have num_blocks entries")
+        _check(_lib.cw_pool_create(int(num_blocks), None if fo is None else _ptr(fo, ctypes.c_int32),
+                                   ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            _lib.cw_pool_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def clone(self) -> "Pool":
+        h = _vp()
+        _check(_lib.cw_pool_clone(self._h, ctypes.byref(h)))
+        return Pool(_handle=h)
+
+    @property
+    def num_free(self) -> int:
+        return int(_lib.cw_pool_num_free(self._h))
+
+    def prefix_match(self, hashes, max_match: int) -> np.ndarray:
+        hs = np.ascontiguousarray(hashes, dtype=np.uint64)
+        ids = np.zeros(len(hs), dtype=np.int32)
+        depth = ctypes.c_int32(0)
+        _check(_lib.cw_prefix_match(self._h, _ptr(hs, ctypes.c_uint64), len(hs), int(max_match),
+                                    _ptr(ids, ctypes.c_int32), ctypes.byref(depth)))
+        return ids[:depth.value].copy()
+
+    def alloc(self, n: int) -> np.ndarray:
+        ids = np.zeros(max(0, int(n)), dtype=np.int32)
+        _check(_lib.cw_pool_alloc(self._h, int(n), _ptr(ids, ctypes.c_int32)))
+        return ids
+
+    def commit(self, hashes, block_ids) -> None:
+        hs = np.ascontiguousarray(hashes, dtype=np.uint64)
+        ids = _i32_array(block_ids, "block_ids")
+        if len(hs) != len(ids):
+            raise ValueError("hashes and block_ids differ in length")
+        _check(_lib.cw_pool_commit(self._h, _ptr(hs, ctypes.c_uint64), _ptr(ids, ctypes.c_int32), len(ids)))
+
+    def release(self, block_ids) -> None:
+        ids = _i32_array(block_ids, "block_ids")
+        _check(_lib.cw_pool_release(self._h, _ptr(ids, ctypes.c_int32), len(ids)))
+
+
+def schedule_batch(pool: Pool, prompts, bt_stride: int, block_size: int = BLOCK_SIZE):
+    """cw_schedule_batch over a list of token arrays.
+
+    Returns (block_table [B, bt_stride], prefix_len [B], cu_suffix [B + 1]) as int32."""
+    toks = [_i32_array(p, "tokens") for p in prompts]
+    cu_tokens = np.zeros(len(toks) + 1, dtype=np.int64)
+    cu_tokens[1:] = np.cumsum([len(t) for t in toks])
+    flat = np.ascontiguousarray(np.concatenate(toks) if toks else np.zeros(0, np.int32), dtype=np.int32)
+    B = len(toks)
+    bt = np.zeros((B, bt_stride), dtype=np.int32)
+    plen = np.zeros(B, dtype=np.int32)
+    cu = np.zeros(B + 1, dtype=np.int32)
+    _check(_lib.cw_schedule_batch(pool.handle, _ptr(flat, ctypes.c_int32), _ptr(cu_tokens, ctypes.c_int64),
+                                  B, block_size, bt_stride, _ptr(bt, ctypes.c_int32),
+                                  _ptr(plen, ctypes.c_int32), _ptr(cu, ctypes.c_int32)))
+    return bt, plen, cu
+
+
+def release_batch(pool: Pool, block_table, prefix_len, cu_suffix, block_size: int = BLOCK_SIZE) -> None:
+    bt = _i32_array(block_table, "block_table")
+    plen = _i32_array(prefix_len, "prefix_len")
+    cu = _i32_array(cu_suffix, "cu_suffix")
+    _check(_lib.cw_release_batch(pool.handle, _ptr(bt, ctypes.c_int32), bt.shape[1], _ptr(plen, ctypes.c_int32),
+                                 _ptr(cu, ctypes.c_int32), len(plen), block_size))
+
+
+def suffix_prefill_plan(cu_suffix, prefix_len, num_q_heads: int, num_kv_heads: int, head_dim: int):
+    """cw_suffix_prefill_plan: returns (plan int32 array, num_tiles)."""
+    cu = _i32_array(cu_suffix, "cu_suffix")
+    plen = _i32_array(prefix_len, "prefix_len")
+    B = len(plen)
+    words = int(_lib.cw_suffix_prefill_plan_words(_ptr(cu, ctypes.c_int32), _ptr(plen, ctypes.c_int32), B,
+                                                  num_q_heads, num_kv_heads, head_dim))
+    if words < 0:
+        _check(words)
+    plan = np.zeros(max(words, 4), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(_lib.cw_suffix_prefill_plan(_ptr(cu, ctypes.c_int32), _ptr(plen, ctypes.c_int32), B, num_q_heads,
+                                       num_kv_heads, head_dim, _ptr(plan, ctypes.c_int32), len(plan),
+                                       ctypes.byref(n)))
+    return plan[:4 * n.value].copy(), n.value
+
+
+# ---------------------------------------------------------------- device calls
+def _dev(t: torch.Tensor, dtype, name: str) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be in GPU memory")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+class BatchMeta:
+    """Host and device copies of a ragged batch's description.
+
+    block_table [B, stride], cu_suffix [B + 1], prefix_len [B] (int32); the
+    plan is built on the host by the library. With device=None nothing is
+    uploaded and the caller assigns the device tensors bt, cu, plen, plan."""
+
+    def __init__(self, block_table, cu_suffix, prefix_len, num_q_heads: int, num_kv_heads: int,
+                 head_dim: int, device="cuda"):
+        self.bt_host = _i32_array(block_table, "block_table")
+        self.cu_host = _i32_array(cu_suffix, "cu_suffix")
+        self.plen_host = _i32_array(prefix_len, "prefix_len")
+        if self.bt_host.ndim != 2 or self.bt_host.shape[0] != len(self.plen_host):
+            raise ValueError("block_table must be [batch, stride]")
+        if len(self.cu_host) != len(self.plen_host) + 1:
+            raise ValueError("cu_suffix must have batch + 1 entries")
+        self.batch = len(self.plen_host)
+        self.num_q_heads, self.num_kv_heads, self.head_dim = num_q_heads, num_kv_heads, head_dim
+        self.plan_host, self.num_tiles = suffix_prefill_plan(self.cu_host, self.plen_host, num_q_heads,
+                                                             num_kv_heads, head_dim)
+        self.device = device
+        self.bt = self.cu = self.plen = self.plan = None
+        if device is not None:
+            self.bt = torch.from_numpy(self.bt_host).to(device)
+            self.cu = torch.from_numpy(self.cu_host).to(device)
+            self.plen = torch.from_numpy(self.plen_host).to(device)
+            plan = self.plan_host if self.plan_host.size else np.zeros(4, np.int32)
+            self.plan = torch.from_numpy(plan).to(device)
+
+    @property
+    def total_rows(self) -> int:
+        return int(self.cu_host[-1])
+
+    @property
+    def bt_stride(self) -> int:
+        return int(self.bt_host.shape[1])
+
+    def _hp(self, a):
+        return _ptr(a, ctypes.c_int32)
+
+
+def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor,
+              v_cache: torch.Tensor, stream=None) -> None:
+    """cw_kv_append: write the suffix K/V rows into their cache blocks."""
+    hkv, D = meta.num_kv_heads, meta.head_dim
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        if tuple(t.shape) != (meta.total_rows, hkv, D):
+            raise ValueError(f"{name} must be [{meta.total_rows}, {hkv}, {D}], got {tuple(t.shape)}")
+    if k_cache.dim() != 4 or tuple(k_cache.shape[1:]) != (hkv, BLOCK_SIZE, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [num_blocks, Hkv, 16, D]")
+    _check(_lib.cw_kv_append(_dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
+                             _dev(k_cache, torch.bfloat16, "k_cache"), _dev(v_cache, torch.bfloat16, "v_cache"),
+                             _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
+                             _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
+                             meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hkv, D, BLOCK_SIZE,
+                             k_cache.shape[0], _stream(stream)))
+
+
+def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                        softmax_scale: float, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """cw_suffix_prefill_attn: attention of the suffix rows; returns out [total_s, Hq, D] bf16."""
+    hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
+    if tuple(q.shape) != (meta.total_rows, hq, D):
+        raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
+    if k_cache.dim() != 4 or tuple(k_cache.shape[1:]) != (hkv, BLOCK_SIZE, D) or v_cache.shape != k_cache.shape:
+        raise ValueError("caches must be [num_blocks, Hkv, 16, D]")
+    if out is None:
+        out = torch.empty_like(q)
+    elif tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must have q's shape")
+    _check(_lib.cw_suffix_prefill_attn(
+        _dev(q, torch.bfloat16, "q"), _dev(k_cache, torch.bfloat16, "k_cache"),
+        _dev(v_cache, torch.bfloat16, "v_cache"), _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
+        _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
+        meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
+        k_cache.shape[0], float(softmax_scale), _dev(meta.plan, torch.int32, "plan"), meta.num_tiles,
+        _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out

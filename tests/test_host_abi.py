@@ -1,0 +1,287 @@
+"""Host side of libcw on the CPU: exported symbols, hashes, the block pool,
+batch scheduling, the tile planner and argument validation of the device entry
+points (which fail before touching a GPU). Expected values come from the
+oracle package."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import paged
+from paper_2606_19667_amd import cw, workload as W
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "cw.h")
+
+
+def test_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(cw_[a-z0-9_]+)\s*\(", text))
+    assert declared == set(cw.EXPORTED)
+    lib = ctypes.CDLL(cw.LIB_PATH)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert cw.abi_version() == 1
+
+
+@pytest.mark.parametrize("n", [0, 1, 15, 16, 17, 100, 1408])
+def test_block_hashes_match_oracle(n):
+    toks = np.random.default_rng(n).integers(-2**31, 2**31 - 1, size=n, dtype=np.int64).astype(np.int32)
+    got = cw.block_hashes(toks, 16)
+    assert [int(x) for x in got] == paged.chain_block_hashes(toks, 16)
+
+
+def test_block_hashes_other_block_sizes():
+    toks = np.arange(100, dtype=np.int32)
+    for bs in (1, 7, 32):
+        assert [int(x) for x in cw.block_hashes(toks, bs)] == paged.chain_block_hashes(toks, bs)
+
+
+def _same_error(fn_a, fn_b):
+    ea = eb = None
+    ra = rb = None
+    try:
+        ra = fn_a()
+    except cw.CwError as e:
+        ea = e.status
+    try:
+        rb = fn_b()
+    except ValueError:
+        eb = "err"
+    assert (ea is None) == (eb is None), (ea, eb)
+    return ra, rb
+
+
+def test_pool_matches_oracle_on_random_operations():
+    rng = np.random.default_rng(11)
+    for trial in range(20):
+        nb = int(rng.integers(4, 40))
+        order = rng.permutation(nb)
+        c = cw.Pool(nb, order)
+        o = paged.PoolSim(nb, order)
+        hash_space = [int(x) for x in rng.integers(1, 2**63, size=12)]
+        held = []
+        for step in range(300):
+            op = rng.integers(0, 4)
+            if op == 0:
+                n = int(rng.integers(0, 6))
+                a, b = _same_error(lambda: c.alloc(n), lambda: o.alloc(n))
+                if a is not None:
+                    assert a.tolist() == b
+                    held += b
+            elif op == 1:
+                hs = [hash_space[int(i)] for i in rng.integers(0, len(hash_space), size=int(rng.integers(0, 5)))]
+                cap = int(rng.integers(0, 6))
+                a = c.prefix_match(hs, cap)
+                b = o.prefix_match(hs, cap)
+                assert a.tolist() == b
+                held += b
+            elif op == 2 and held:
+                k = int(rng.integers(1, min(4, len(held)) + 1))
+                ids = [held[int(i)] for i in rng.choice(len(held), size=k, replace=False)]
+                if rng.random() < 0.1:
+                    ids = ids + [int(rng.integers(0, nb))]
+                hs = [hash_space[int(i)] for i in rng.integers(0, len(hash_space), size=len(ids))]
+                _same_error(lambda: c.commit(hs, ids), lambda: o.commit(hs, ids))
+            elif op == 3 and held:
+                k = int(rng.integers(1, min(4, len(held)) + 1))
+                idx = sorted(rng.choice(len(held), size=k, replace=False).tolist(), reverse=True)
+                ids = [held[i] for i in idx]
+                if rng.random() < 0.1:
+                    ids = ids + [int(rng.integers(0, nb))]
+                a, b = _same_error(lambda: c.release(ids), lambda: o.release(ids))
+                if a is None and b is None and not isinstance(a, Exception):
+                    pass
+                if o.ref == [int(x) for x in o.ref]:
+                    pass
+                # keep `held` in sync with the oracle's counts
+                held = [b2 for b2 in range(nb) for _ in range(o.ref[b2])]
+            assert c.num_free == len(o.free)
+        # the free-queue order decides future allocations
+        assert c.alloc(c.num_free).tolist() == o.alloc(len(o.free))
+
+
+def _simulate_oracle(prompts, pool, bs, stride):
+    tables, plens, cus = [], [], [0]
+    for toks in prompts:
+        hs = paged.chain_block_hashes(toks, bs)
+        ids = pool.prefix_match(hs, (len(toks) - 1) // bs)
+        new = pool.alloc(math.ceil(len(toks) / bs) - len(ids))
+        pool.commit(hs[len(ids):], new[:len(hs) - len(ids)])
+        row = ids + new
+        tables.append(row + [-1] * (stride - len(row)))
+        plens.append(len(ids) * bs)
+        cus.append(cus[-1] + len(toks) - len(ids) * bs)
+    return np.array(tables, np.int32), np.array(plens, np.int32), np.array(cus, np.int32)
+
+
+def test_schedule_batch_matches_oracle_on_trace():
+    w = W.llama8b_trace_batch(seed=0, batch=16, warmup=48)
+    prompts = [p.tokens(w.seed) for p in w.warmup + w.prompts]
+    nb = w.num_blocks()
+    order = w.free_order()
+    c = cw.Pool(nb, order)
+    o = paged.PoolSim(nb, order)
+    stride = 88
+    for toks in prompts[:len(w.warmup)]:
+        bt, pl, cu = cw.schedule_batch(c, [toks], stride)
+        ebt, epl, ecu = _simulate_oracle([toks], o, 16, stride)
+        assert np.array_equal(bt, ebt) and np.array_equal(pl, epl) and np.array_equal(cu, ecu)
+        cw.release_batch(c, bt, pl, cu)
+        o.release([b for b in ebt[0] if b >= 0])
+    batch = prompts[len(w.warmup):]
+    bt, pl, cu = cw.schedule_batch(c, batch, stride)
+    ebt, epl, ecu = _simulate_oracle(batch, o, 16, stride)
+    assert np.array_equal(bt, ebt) and np.array_equal(pl, epl) and np.array_equal(cu, ecu)
+    # depths are whole documents past the instruction; the greedy depth is a lower bound
+    for p, d in zip(pl, w.trie_depths):
+        assert (p - 64) % 256 == 0 and p >= 64 + 256 * d
+    cw.release_batch(c, bt, pl, cu)
+
+
+def test_schedule_batch_rolls_back_on_exhaustion():
+    c = cw.Pool(10)
+    a = c.alloc(3)
+    c.commit([1, 2, 3], a)
+    c.release(a)
+    snap = c.clone()
+    prompts = [np.arange(48, dtype=np.int32), np.arange(1000, 1000 + 16 * 9, dtype=np.int32)]
+    with pytest.raises(cw.CwError) as e:
+        cw.schedule_batch(c, prompts, 16)
+    assert e.value.status == cw.CW_ENOSPC
+    assert c.num_free == snap.num_free == 10
+    assert c.alloc(10).tolist() == snap.alloc(10).tolist()
+
+
+def test_schedule_batch_keeps_one_suffix_token_and_shares_within_batch():
+    c = cw.Pool(64)
+    p = np.arange(64, dtype=np.int32)
+    bt, pl, cu = cw.schedule_batch(c, [p, p, np.concatenate([p, [7]])], 8)
+    assert pl.tolist() == [0, 48, 64]          # cap (L-1)//16 blocks; same-batch reuse
+    assert cu.tolist() == [0, 64, 80, 81]
+    assert bt[1, :3].tolist() == bt[0, :3].tolist() and bt[2, :4].tolist() == bt[0, :4].tolist()
+    assert bt[0, 4:].tolist() == [-1] * 4
+
+
+def _plan_rows(plan, ntiles, cu, hkv, per):
+    seen = {}
+    for i in range(ntiles):
+        r, g, row0, cost = plan[4 * i:4 * i + 4]
+        if r < 0:
+            continue
+        S = cu[r + 1] - cu[r]
+        for row in range(row0, min(S, row0 + per)):
+            key = (r, g, row)
+            seen[key] = seen.get(key, 0) + 1
+    return seen
+
+
+@pytest.mark.parametrize("shape", [(4, 1), (32, 8), (64, 8), (28, 4)])
+def test_plan_covers_every_row_once(shape):
+    hq, hkv = shape
+    rng = np.random.default_rng(hq)
+    for B in (1, 3, 16, 40):
+        S = rng.integers(0, 700, size=B)
+        S[0] = max(S[0], 1)
+        P = rng.integers(0, 60, size=B) * 16
+        cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
+        plan, n = cw.suffix_prefill_plan(cu, P, hq, hkv, 128)
+        per = 128 // (hq // hkv)
+        seen = _plan_rows(plan, n, cu, hkv, per)
+        assert len(seen) == int(S.sum()) * hkv and set(seen.values()) == {1}
+        real = [plan[4 * i:4 * i + 4] for i in range(n) if plan[4 * i] >= 0]
+        assert len(real) == sum(math.ceil(s / per) for s in S) * hkv
+        for t in real:
+            r, g, row0, cost = t
+            kv_end = P[r] + row0 + min(per, S[r] - row0)
+            assert cost == math.ceil(kv_end / 64)
+        # every L2-partition queue (entries i % 8) is heaviest first
+        if n > len(real) or B * hkv >= 32:
+            for x in range(8):
+                costs = [plan[4 * i + 3] for i in range(x, n, 8) if plan[4 * i] >= 0]
+                assert costs == sorted(costs, reverse=True)
+        else:
+            costs = [t[3] for t in real]
+            assert costs == sorted(costs, reverse=True)
+
+
+def test_plan_groups_pairs_on_one_partition():
+    cu = np.arange(0, 17 * 576, 576, dtype=np.int32)
+    P = np.full(16, 832, np.int32)
+    plan, n = cw.suffix_prefill_plan(cu, P, 32, 8, 128)
+    part = {}
+    for i in range(n):
+        r, g = plan[4 * i], plan[4 * i + 1]
+        if r >= 0:
+            assert part.setdefault((r, g), i % 8) == i % 8
+
+
+def _dummy():
+    return ctypes.c_void_p(16)
+
+
+def _arr(x):
+    a = np.ascontiguousarray(x, np.int32)
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _attn(cu, plen, hq=32, hkv=8, d=128, bs=16, stride=100, scale=0.1, ntiles=None, nb=100):
+    cu_a, cu_p = _arr(cu)
+    pl_a, pl_p = _arr(plen)
+    if ntiles is None:
+        per = max(1, 128 // max(1, hq // hkv))
+        ntiles = sum(math.ceil((cu[i + 1] - cu[i]) / per) for i in range(len(plen))) * hkv
+    d_ = _dummy()
+    return cw.lib().cw_suffix_prefill_attn(d_, d_, d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d,
+                                           bs, nb, scale, d_, ntiles, d_, None)
+
+
+def _append(cu, plen, hkv=8, d=128, bs=16, stride=100, nb=100):
+    cu_a, cu_p = _arr(cu)
+    pl_a, pl_p = _arr(plen)
+    d_ = _dummy()
+    return cw.lib().cw_kv_append(d_, d_, d_, d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hkv, d, bs, nb, None)
+
+
+def test_device_entry_points_validate_before_launch():
+    E, U = cw.CW_EINVAL, cw.CW_EUNSUPPORTED
+    assert _attn([0, 10], [8]) == E                       # prefix not a multiple of 16
+    assert _attn([0, 10, 5], [0, 0]) == E                 # cu decreasing
+    assert _attn([1, 10], [0]) == E                       # cu[0] != 0
+    assert _attn([0, 1000], [16 * 90]) == E               # needs more blocks than the stride
+    assert _attn([0, 10], [0], hq=30, hkv=8) == E         # Hq % Hkv
+    assert _attn([0, 10], [0], d=96) == U                 # head_dim
+    assert _attn([0, 10], [0], bs=32) == U                # block size
+    assert _attn([0, 10], [0], hq=256, hkv=1) == U        # group > 128
+    assert _attn([0, 10], [0], ntiles=3) == E             # plan does not match
+    assert _attn([0, 10], [0], scale=float("nan")) == E
+    assert _attn([0, 10], [0], scale=-1.0) == E
+    assert _attn([0, 10], [0], nb=0) == E
+    assert "prefix_len" in cw.last_error() or "num_blocks" in cw.last_error()
+    assert _append([0, 10], [8]) == E
+    assert _append([0, 10], [0], d=80) == U
+    assert _append([0, 10], [0], bs=8) == U
+    assert _append([0, 10], [0], hkv=0) == E
+    assert _append([0, 1000], [16 * 90]) == E
+    assert _attn([0, 0], [0], ntiles=0) == cw.CW_OK       # nothing to do: no launch
+    assert _append([0, 0], [16]) == cw.CW_OK
+
+
+def test_host_calls_reject_bad_arguments():
+    with pytest.raises(cw.CwError):
+        cw.Pool(0)
+    with pytest.raises(cw.CwError):
+        cw.Pool(3, [0, 0, 1])
+    p = cw.Pool(4)
+    with pytest.raises(cw.CwError) as e:
+        p.alloc(5)
+    assert e.value.status == cw.CW_ENOSPC and p.num_free == 4
+    with pytest.raises(cw.CwError):
+        p.release([0])
+    a = p.alloc(2)
+    with pytest.raises(cw.CwError):
+        p.commit([5, 6], [a[0], a[0]])
+    with pytest.raises(cw.CwError):
+        cw.suffix_prefill_plan([0, 10], [0], 32, 8, 96)
