@@ -44,7 +44,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 def attention_flops(prefix_len, suffix_len, hq, d) -> int:
     pairs = sum(int(s) * int(p) + int(s) * (int(s) + 1) // 2 for p, s in zip(prefix_len, suffix_len))
-    return 4 * d * hq * pairs
+    return int(4 * d * hq * pairs)
 
 
 def attention_bytes(prefix_len, suffix_len, hq, hkv, d) -> int:
@@ -52,13 +52,14 @@ def attention_bytes(prefix_len, suffix_len, hq, hkv, d) -> int:
     every request's K and V read once (prefix and suffix)."""
     tot = 0
     for p, s in zip(prefix_len, suffix_len):
+        p, s = int(p), int(s)
         tot += 2 * s * hq * d * 2 + 2 * (p + s) * hkv * d * 2
     return tot
 
 
 def append_bytes(suffix_len, hkv, d) -> int:
     """kv_append: read the new K and V rows, write them into the cache."""
-    return 2 * 2 * int(sum(suffix_len)) * hkv * d * 2
+    return int(2 * 2 * int(sum(suffix_len)) * hkv * d * 2)
 
 
 def make_workload(name: str, seed: int):
@@ -82,19 +83,14 @@ def cpu_baseline(w, sched, budget_s: float = 12.0):
     from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import attention as OA
-    from paper_2606_19667_amd import batch as B
+    from paper_2606_19667_amd.workload import logical_kv, suffix_q
 
     cores = len(os.sched_getaffinity(0))
-    db_host = None
-    flops = 0
-    tokens = 0
-    n = 0
+    flops = tokens = n = 0
     elapsed = 0.0
     with threadpool_limits(limits=cores):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        order = list(range(w.batch))
-        for r in order:
-            from paper_2606_19667_amd.workload import logical_kv, suffix_q
+        for r in range(w.batch):
             P = int(sched.prefix_len[r])
             k, v = logical_kv(w, w.prompts[r])
             q = suffix_q(w, w.prompts[r], P)
@@ -107,10 +103,22 @@ def cpu_baseline(w, sched, budget_s: float = 12.0):
             n += 1
             if elapsed >= budget_s:
                 break
-    del db_host, B
-    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle", "sample": f"{n} of {w.batch} requests, all heads and rows, fp64 NumPy",
-            "seconds": round(elapsed, 3), "suffix_tokens_per_s": tokens / elapsed}
+    return {"value": round(flops / elapsed / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "sample": f"{n} of {w.batch} requests (all heads and rows), fp64 NumPy",
+            "seconds": round(elapsed, 3), "suffix_tokens_per_s": round(tokens / elapsed, 1)}
+
+
+def copy_calibration(mbytes: int, reps: int = 5) -> None:
+    """A plain device copy of `mbytes` MiB, `reps` times: the reference kernel
+    whose FETCH_SIZE / WRITE_SIZE readings scale the attention kernel's."""
+    import torch
+    n = mbytes * (1 << 20) // 2
+    a = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_MiB": mbytes, "reps": reps}), flush=True)
 
 
 def main() -> int:
@@ -121,6 +129,8 @@ def main() -> int:
     ap.add_argument("--workload", default="llama8b-trace-b16")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
+                    help="only run a plain device copy of this size (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -136,6 +146,9 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return 0
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     print(f"[bench] setting up {args.workload}", file=sys.stderr, flush=True)
@@ -264,7 +277,7 @@ def main() -> int:
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                      "kernel": "suffix_prefill_attn_kernel<128>",
-                     "algorithmic_bytes": attention_bytes(P, S, hq, hkv, D)},
+                     "algorithmic_bytes": int(attention_bytes(P, S, hq, hkv, D))},
     }
     del db
     torch.cuda.empty_cache()

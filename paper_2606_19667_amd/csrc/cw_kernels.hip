@@ -28,6 +28,7 @@
 #include <cmath>
 #include <cstdint>
 #include <string>
+#include <type_traits>
 
 #include "cw_internal.h"
 
@@ -88,11 +89,38 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 
 // ---------------------------------------------------------------------------
 // Suffix prefill attention.
+//
+// LDS holds two K/V stages (double buffering, one barrier per 64-key step).
+// The next step's K/V are fetched into registers while the current step is
+// computed, then written into the other stage.
+//  * K: row-major [key][d], rows padded by 16 bytes, so the 16-row groups of
+//    the QK^T operand reads fall on distinct banks.
+//  * V: row-major [key][d] with the 16-byte chunks of each row XOR-swizzled by
+//    fv(row), spreading the eight rows one transposing read touches over all
+//    chunk groups. V feeds the PV MFMA through ds_read_b64_tr_b16: in each
+//    16-lane group, lane o receives element o % 4 of the 8-byte pieces addressed
+//    by lanes o / 4 + 4 j, j = 0..3; so lane i addresses key (base + i / 4),
+//    d (base + 4 (i % 4)), and lane o receives d = base + o for four keys.
 // ---------------------------------------------------------------------------
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
+typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
+
 template <int D>
-struct AttnSmem {
-  uint16_t k[kKv][D + 8];    // keys, row-major; 16-byte pad staggers LDS banks
-  uint16_t vt[D][kKv + 4];   // values transposed to [d][key]; 8-byte pad
+struct AttnGeom {
+  static constexpr int RB = 2 * D;              // bytes per K/V row in global memory
+  static constexpr int KRB = RB + 16;           // padded K row in LDS
+  static constexpr int NC = D / 8;              // 16-byte chunks per row
+  static constexpr int KTILE = kKv * KRB;
+  static constexpr int VTILE = kKv * RB;
+  static constexpr int STAGE = KTILE + VTILE;
+  static constexpr int RPL = 1024 / RB;         // rows covered by one wave-wide 16-byte load
+  static constexpr int LPW = kBs / RPL;         // loads per wave per tensor (one block)
+  static constexpr int KS = D / 16;             // MFMA k-steps over D
+  static constexpr int DT = D / 32;             // 32-row output tiles over D
+  __device__ static int vswz(int row) {
+    return D == 128 ? (4 * (row & 3) + ((row >> 2) & 3)) : (row & (NC - 1));
+  }
 };
 
 template <int D>
@@ -103,15 +131,9 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
                                 const int32_t* __restrict__ plen, const int4* __restrict__ plan,
                                 int batch, int hq, int hkv, int group, int per_tile, int num_blocks,
                                 float c_log2, uint16_t* __restrict__ out) {
-  constexpr int CPR = D / 8;                    // 16-byte chunks per key row
-  constexpr int KCH = kKv * CPR / kThreads;     // K chunks per thread per tile
-  constexpr int VK = kKv * CPR / kThreads;      // consecutive V keys per thread
-  constexpr int KROWS = kThreads / CPR;         // key rows covered per K chunk step
-  constexpr int KS = D / 16;                    // MFMA k-steps over D
-  constexpr int DT = D / 32;                    // 32-row output tiles over D
-  static_assert(KCH * kThreads == kKv * CPR && VK * (kThreads / CPR) == kKv, "tile split");
-
-  __shared__ AttnSmem<D> sm;
+  using G = AttnGeom<D>;
+  constexpr int KS = G::KS, DT = G::DT, RB = G::RB, KRB = G::KRB, NC = G::NC, LPW = G::LPW;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * G::STAGE];
 
   const int4 item = plan[blockIdx.x];
   const int r = item.x, g = item.y, row0 = item.z;
@@ -124,13 +146,14 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   const int nvalid = min(per_tile, S - row0);
   const int kv_end = P + row0 + nvalid;
   const int ntiles = (kv_end + kKv - 1) / kKv;
+  const int nblk = (L + kBs - 1) / kBs;
   const int32_t* btr = bt + int64_t(r) * bt_stride;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
   const int l32 = lane & 31;
   const int half = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // This lane's query column.
   const int m = wave * 32 + l32;
@@ -151,138 +174,163 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
     for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
   }
 
-  // Staging registers for one K/V tile.
-  u32x4 ks[KCH];
-  u32x4 vs[VK];
-  const int dc = tid % CPR;
-  const int vkey0 = (tid / CPR) * VK;
+  // ---- K/V staging. Wave w fetches block w of each 64-key step: LPW 16-byte
+  // loads per tensor per lane, lane l of load i reading row RPL i + l / NC,
+  // chunk l % NC (one contiguous 1 KB run per load).
+  // Physical block of logical block lb, or -1 past the prompt / outside the
+  // pool; the table index is clamped into the request's row (always in bounds).
+  auto block_id = [&](int lb) -> int {
+    const int b = btr[min(lb, nblk - 1)];
+    return (lb < nblk && b >= 0 && b < num_blocks) ? b : -1;
+  };
+  const int ld_row = lane / NC;
+  const int ld_ch = lane % NC;
+  u32x4 kreg[LPW], vreg[LPW];
+  auto fetch = [&](int b) {
+    const int bb = b < 0 ? 0 : b;   // block 0 stands in for a missing block; zeroed when staged
+    const uint8_t* kb = reinterpret_cast<const uint8_t*>(kc) + (int64_t(bb) * hkv + g) * (kBs * RB);
+    const uint8_t* vb = reinterpret_cast<const uint8_t*>(vc) + (int64_t(bb) * hkv + g) * (kBs * RB);
+    const int off = ld_row * RB + ld_ch * 16;
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      kreg[i] = *reinterpret_cast<const u32x4*>(kb + off + i * 1024);
+      vreg[i] = *reinterpret_cast<const u32x4*>(vb + off + i * 1024);
+    }
+  };
+  // Rows of a missing block and rows past the prompt end are written as zeros
+  // (stale cache bytes must never meet a zero probability).
+  auto stage_write = [&](uint8_t* st, int k0, int b) {
+    const int key0 = k0 + kBs * wave;
+    const bool full = b >= 0 && key0 + kBs <= L;   // wave-uniform fast path
+    const u32x4 zero{0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      const int row = kBs * wave + G::RPL * i + ld_row;
+      const bool ok = full || (b >= 0 && key0 + G::RPL * i + ld_row < L);
+      *reinterpret_cast<u32x4*>(st + row * KRB + ld_ch * 16) = ok ? kreg[i] : zero;
+      *reinterpret_cast<u32x4*>(st + G::KTILE + row * RB + ((ld_ch ^ G::vswz(row)) << 4)) = ok ? vreg[i] : zero;
+    }
+  };
 
-  auto block_of = [&](int key) -> int {
-    if (key >= L) return -1;
-    const int b = btr[key >> 4];
-    return (b >= 0 && b < num_blocks) ? b : -1;
-  };
-  auto fetch = [&](int k0) {
+  // ---- per-lane LDS read offsets (relative to a stage)
+  // K operand: row st*32 + l32, chunk 2s + half.
+  const int k_off = l32 * KRB + half * 16;
+  // V operand (transposing read): group gi = lane / 16, i = lane % 16:
+  //   key = 16 kk + 8 sel + 4 (gi / 2) + i / 4,  d = 32 t + 16 (gi % 2) + 4 (i % 4).
+  // vswz(key) depends on key mod 16 only, so kk enters as a constant offset.
+  const int gi = lane >> 4, li = lane & 15;
+  const int vkey_l = 4 * (gi >> 1) + (li >> 2);
+  const int vd_l = 16 * (gi & 1) + 4 * (li & 3);
+  int v_off[DT][2];
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int key = k0 + tid / CPR + KROWS * i;
-      const int b = block_of(key);
-      ks[i] = b < 0 ? u32x4{0, 0, 0, 0}
-                    : *reinterpret_cast<const u32x4*>(
-                          kc + ((int64_t(b) * hkv + g) * kBs + (key & (kBs - 1))) * D + dc * 8);
+  for (int t = 0; t < DT; ++t)
+#pragma unroll
+    for (int sel = 0; sel < 2; ++sel) {
+      const int key = 8 * sel + vkey_l;
+      const int d = 32 * t + vd_l;
+      v_off[t][sel] = G::KTILE + key * RB + (((d >> 3) ^ G::vswz(key)) << 4) + ((d & 4) << 1);
     }
-#pragma unroll
-    for (int j = 0; j < VK; ++j) {
-      const int key = k0 + vkey0 + j;
-      const int b = block_of(key);
-      vs[j] = b < 0 ? u32x4{0, 0, 0, 0}
-                    : *reinterpret_cast<const u32x4*>(
-                          vc + ((int64_t(b) * hkv + g) * kBs + (key & (kBs - 1))) * D + dc * 8);
-    }
-  };
-  auto stage = [&]() {
-#pragma unroll
-    for (int i = 0; i < KCH; ++i)
-      *reinterpret_cast<u32x4*>(&sm.k[tid / CPR + KROWS * i][dc * 8]) = ks[i];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const int d = dc * 8 + 2 * w;
-      if constexpr (VK == 4) {
-        const u32x2 lo{(vs[0][w] & 0xFFFFu) | (vs[1][w] << 16), (vs[2][w] & 0xFFFFu) | (vs[3][w] << 16)};
-        const u32x2 hi{(vs[0][w] >> 16) | (vs[1][w] & 0xFFFF0000u), (vs[2][w] >> 16) | (vs[3][w] & 0xFFFF0000u)};
-        *reinterpret_cast<u32x2*>(&sm.vt[d][vkey0]) = lo;
-        *reinterpret_cast<u32x2*>(&sm.vt[d + 1][vkey0]) = hi;
-      } else {
-        *reinterpret_cast<uint32_t*>(&sm.vt[d][vkey0]) = (vs[0][w] & 0xFFFFu) | (vs[1][w] << 16);
-        *reinterpret_cast<uint32_t*>(&sm.vt[d + 1][vkey0]) = (vs[0][w] >> 16) | (vs[1][w] & 0xFFFF0000u);
-      }
-    }
-  };
 
   f32x16 oacc[DT];
 #pragma unroll
   for (int t = 0; t < DT; ++t) oacc[t] = f32x16{};
-  float m_run = -INFINITY;
-  float l_run = 0.f;
+  float m_run = -INFINITY;   // running max (raw score units) used for the exponent
+  float l_run = 0.f;         // this lane's partial row sum (its 32 keys per step)
+  const bf16x2 ones{(__bf16)1.0f, (__bf16)1.0f};
+  // Lazy rescaling: the exponent base m_run moves only when a score exceeds it
+  // by more than 2^8 in probability, so O and l are rarely rescaled.
+  const float lazy = 8.0f / c_log2;
 
-  fetch(0);
-  for (int it = 0; it < ntiles; ++it) {
-    const int k0 = it * kKv;
-    __syncthreads();
-    stage();
-    __syncthreads();
-    if (it + 1 < ntiles) fetch(k0 + kKv);
-
-    // S^T = K Q^T for keys k0 .. k0+63 (two 32-key halves).
-    f32x16 sacc[2];
+  auto compute = [&](const uint8_t* st, int k0) {
+    // S^T = K Q^T for keys k0 .. k0 + 63 (two 32-key halves).
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      sacc[st] = f32x16{};
+    for (int s = 0; s < KS; ++s)
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
+      for (int h = 0; h < 2; ++h) {
         const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(&sm.k[st * 32 + l32][s * 16 + half * 8]));
-        sacc[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[st], 0, 0, 0);
+            bf16x8, *reinterpret_cast<const u32x4*>(st + k_off + h * 32 * KRB + s * 32));
+        sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[h], 0, 0, 0);
       }
-    }
-
-    // Causal mask, only where the tile reaches past the first row's limit.
+    // Causal mask, only where the step reaches past the first row's limit.
     if (k0 + kKv - 1 > P + row0) {
+      const int lim = qpos - k0;
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int key = k0 + st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-          if (key > qpos) sacc[st][e] = -INFINITY;
+          const int key = h * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+          if (key > lim) sacc[h][e] = -INFINITY;
         }
     }
-
     float mx = -INFINITY;
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[st][e]);
+      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[h][e], sacc[h][e + 1]));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);          // finite: key 0 is visible to every row
-    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
-    const float mc = m_new * c_log2;
-    float lsum = 0.f;
+    // key 0 is visible to every row, so after the first step m_run is finite
+    const bool grow = !(mx <= m_run + lazy);
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float m_new = grow ? fmaxf(mx, m_run) : m_run;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
+      l_run *= alpha;
 #pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[st][e], c_log2, -mc));
-        sacc[st][e] = p;
-        lsum += p;
-      }
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
-
-    // P^T as the B operand: slice kk holds keys 16kk .. 16kk+15.
+      for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = m_run * c_log2;
     bf16x8 pb[4];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const int st = kk >> 1, e0 = (kk & 1) * 8;
-      const u32x4 w{pack_bf16x2(sacc[st][e0 + 0], sacc[st][e0 + 1]),
-                    pack_bf16x2(sacc[st][e0 + 2], sacc[st][e0 + 3]),
-                    pack_bf16x2(sacc[st][e0 + 4], sacc[st][e0 + 5]),
-                    pack_bf16x2(sacc[st][e0 + 6], sacc[st][e0 + 7])};
-      pb[kk] = __builtin_bit_cast(bf16x8, w);
+      const int h = kk >> 1, e0 = (kk & 1) * 8;
+      uint32_t w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[h][e0 + 2 * j], c_log2, -mc));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[h][e0 + 2 * j + 1], c_log2, -mc));
+        w[j] = pack_bf16x2(p0, p1);
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[j]), ones, l_run, false);
+      }
+      pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
-
     // O^T += V^T P^T
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const uint16_t* vrow = &sm.vt[t * 32 + l32][16 * kk + 4 * half];
-        const u32x2 a0 = *reinterpret_cast<const u32x2*>(vrow);
-        const u32x2 a1 = *reinterpret_cast<const u32x2*>(vrow + 8);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{a0[0], a0[1], a1[0], a1[1]});
+        const i16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4_t*)((lds_u8_t*)st + v_off[t][0] + kk * 16 * RB));
+        const i16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4_t*)((lds_u8_t*)st + v_off[t][1] + kk * 16 * RB));
+        const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
         oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], oacc[t], 0, 0, 0);
       }
+  };
+
+  // One step: fetch the next step's K/V into registers, compute this step from
+  // stage SI, write the registers into the other stage, then one barrier.
+  int b_next = block_id(wave);
+  fetch(b_next);
+  stage_write(lds, 0, b_next);
+  if (ntiles > 1) b_next = block_id(kKv / kBs + wave);
+  __syncthreads();
+  auto step = [&](auto si, int it) {
+    constexpr int SI = decltype(si)::value;
+    const int k0 = it * kKv;
+    const bool more = it + 1 < ntiles;
+    const int b = b_next;
+    if (more) {
+      fetch(b);
+      if (it + 2 < ntiles) b_next = block_id((k0 + 2 * kKv) / kBs + wave);
+    }
+    compute(lds + SI * G::STAGE, k0);
+    if (more) stage_write(lds + (1 - SI) * G::STAGE, k0 + kKv, b);
+    __syncthreads();
+  };
+  for (int it = 0; it < ntiles; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
