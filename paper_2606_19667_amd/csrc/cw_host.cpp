@@ -645,51 +645,55 @@ PlanShape plan_shape(const int32_t* cu, const int32_t* plen, int32_t batch, int3
 // Writes the plan: 4 int32 per entry {request, kv head, first row, cost}.
 void write_plan(const PlanShape& ps, const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hkv,
                 int32_t* out) {
-  const int nq = ps.part.empty() ? 1 : cw::kNumXcd;
-  const int32_t nc = ps.max_cost + 1;
-  // Counting sort by (queue, cost descending); ties keep generation order
-  // (request, first row, KV head).
-  std::vector<int64_t> start(size_t(nq) * nc, 0);
-  auto queue_of = [&](int32_t r, int32_t g) { return ps.part.empty() ? 0 : int(ps.part[size_t(int64_t(r) * hkv + g)]); };
-  for (int32_t r = 0; r < batch; ++r) {
-    const int32_t S = cu[r + 1] - cu[r];
-    for (int32_t row0 = 0; row0 < S; row0 += ps.per) {
-      const int32_t c = tile_cost(plen[r], row0, S, ps.per);
-      for (int32_t g = 0; g < hkv; ++g) start[size_t(queue_of(r, g)) * nc + (nc - 1 - c)] += 1;
-    }
-  }
-  std::vector<int64_t> qlen(size_t(nq), 0);
-  for (int x = 0; x < nq; ++x) {
-    int64_t acc = 0;
-    for (int32_t k = 0; k < nc; ++k) {
-      const int64_t n = start[size_t(x) * nc + k];
-      start[size_t(x) * nc + k] = acc;
-      acc += n;
-    }
-    qlen[size_t(x)] = acc;
-  }
-  // Queue x, position i  ->  plan entry i * nq + x. Pad first, then fill.
   for (int64_t e = 0; e < ps.padded; ++e) {
     out[4 * e + 0] = -1;
     out[4 * e + 1] = 0;
     out[4 * e + 2] = 0;
     out[4 * e + 3] = 0;
   }
-  for (int32_t r = 0; r < batch; ++r) {
-    const int32_t S = cu[r + 1] - cu[r];
-    for (int32_t row0 = 0; row0 < S; row0 += ps.per) {
-      const int32_t c = tile_cost(plen[r], row0, S, ps.per);
-      for (int32_t g = 0; g < hkv; ++g) {
-        const int x = queue_of(r, g);
-        const int64_t i = start[size_t(x) * nc + (nc - 1 - c)]++;
-        const int64_t e = i * nq + x;
-        out[4 * e + 0] = r;
-        out[4 * e + 1] = g;
-        out[4 * e + 2] = row0;
-        out[4 * e + 3] = c;
+  auto put = [&](int64_t e, int32_t r, int32_t g, int32_t row0) {
+    out[4 * e + 0] = r;
+    out[4 * e + 1] = g;
+    out[4 * e + 2] = row0;
+    out[4 * e + 3] = tile_cost(plen[r], row0, cu[r + 1] - cu[r], ps.per);
+  };
+  if (ps.part.empty()) {
+    // One queue, heaviest first: counting sort by cost; ties keep generation
+    // order (request, first row, KV head).
+    const int32_t nc = ps.max_cost + 1;
+    std::vector<int64_t> start(size_t(nc) + 1, 0);
+    for (int32_t r = 0; r < batch; ++r)
+      for (int32_t row0 = 0, S = cu[r + 1] - cu[r]; row0 < S; row0 += ps.per)
+        start[size_t(nc - 1 - tile_cost(plen[r], row0, S, ps.per)) + 1] += hkv;
+    for (int32_t k = 0; k < nc; ++k) start[size_t(k) + 1] += start[size_t(k)];
+    for (int32_t r = 0; r < batch; ++r)
+      for (int32_t row0 = 0, S = cu[r + 1] - cu[r]; row0 < S; row0 += ps.per) {
+        int64_t& pos = start[size_t(nc - 1 - tile_cost(plen[r], row0, S, ps.per))];
+        for (int32_t g = 0; g < hkv; ++g) put(pos++, r, g, row0);
       }
-    }
+    return;
   }
+  // One queue per L2 partition, pair-major: the partition's (request, KV head)
+  // pairs by total cost (heaviest first), each pair's tiles heaviest (last rows)
+  // first. Only a few pairs are in flight per partition at a time, so their K/V
+  // stay in that partition's L2. Queue x, position i -> entry i * 8 + x.
+  std::vector<int64_t> req_cost(size_t(batch), 0);
+  for (int32_t r = 0; r < batch; ++r)
+    for (int32_t row0 = 0, S = cu[r + 1] - cu[r]; row0 < S; row0 += ps.per)
+      req_cost[size_t(r)] += tile_cost(plen[r], row0, S, ps.per);
+  std::vector<int32_t> order(static_cast<size_t>(batch));
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int32_t a, int32_t b) { return req_cost[size_t(a)] > req_cost[size_t(b)]; });
+  int64_t pos[cw::kNumXcd] = {0};
+  for (int32_t r : order)
+    for (int32_t g = 0; g < hkv; ++g) {
+      const int x = ps.part[size_t(int64_t(r) * hkv + g)];
+      const int32_t S = cu[r + 1] - cu[r];
+      if (S == 0) continue;
+      const int32_t last = ((S - 1) / ps.per) * ps.per;
+      for (int32_t row0 = last; row0 >= 0; row0 -= ps.per) put(pos[x]++ * cw::kNumXcd + x, r, g, row0);
+    }
 }
 
 }  // namespace

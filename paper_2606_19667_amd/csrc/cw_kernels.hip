@@ -201,12 +201,20 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   // (stale cache bytes must never meet a zero probability).
   auto stage_write = [&](uint8_t* st, int k0, int b) {
     const int key0 = k0 + kBs * wave;
-    const bool full = b >= 0 && key0 + kBs <= L;   // wave-uniform fast path
+    if (b >= 0 && key0 + kBs <= L) {   // wave-uniform: the whole block is valid
+#pragma unroll
+      for (int i = 0; i < LPW; ++i) {
+        const int row = kBs * wave + G::RPL * i + ld_row;
+        *reinterpret_cast<u32x4*>(st + row * KRB + ld_ch * 16) = kreg[i];
+        *reinterpret_cast<u32x4*>(st + G::KTILE + row * RB + ((ld_ch ^ G::vswz(row)) << 4)) = vreg[i];
+      }
+      return;
+    }
     const u32x4 zero{0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < LPW; ++i) {
       const int row = kBs * wave + G::RPL * i + ld_row;
-      const bool ok = full || (b >= 0 && key0 + G::RPL * i + ld_row < L);
+      const bool ok = b >= 0 && key0 + G::RPL * i + ld_row < L;
       *reinterpret_cast<u32x4*>(st + row * KRB + ld_ch * 16) = ok ? kreg[i] : zero;
       *reinterpret_cast<u32x4*>(st + G::KTILE + row * RB + ((ld_ch ^ G::vswz(row)) << 4)) = ok ? vreg[i] : zero;
     }

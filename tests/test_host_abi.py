@@ -178,6 +178,17 @@ def _plan_rows(plan, ntiles, cu, hkv, per):
     return seen
 
 
+def _grouped(plan, n, hkv):
+    """True when each (request, KV head) pair sits on one partition (i % 8)."""
+    part = {}
+    for i in range(n):
+        if plan[4 * i] >= 0:
+            key = (plan[4 * i], plan[4 * i + 1])
+            if part.setdefault(key, i % 8) != i % 8:
+                return False
+    return len(part) >= 32
+
+
 @pytest.mark.parametrize("shape", [(4, 1), (32, 8), (64, 8), (28, 4)])
 def test_plan_covers_every_row_once(shape):
     hq, hkv = shape
@@ -197,14 +208,49 @@ def test_plan_covers_every_row_once(shape):
             r, g, row0, cost = t
             kv_end = P[r] + row0 + min(per, S[r] - row0)
             assert cost == math.ceil(kv_end / 64)
-        # every L2-partition queue (entries i % 8) is heaviest first
-        if n > len(real) or B * hkv >= 32:
+        if _grouped(plan, n, hkv):
+            # per L2-partition queue (entries i % 8): pairs contiguous, each pair's
+            # tiles heaviest first, pairs by non-increasing total cost
             for x in range(8):
-                costs = [plan[4 * i + 3] for i in range(x, n, 8) if plan[4 * i] >= 0]
-                assert costs == sorted(costs, reverse=True)
+                q = [tuple(plan[4 * i:4 * i + 4]) for i in range(x, n, 8) if plan[4 * i] >= 0]
+                pairs, totals = [], {}
+                for r_, g_, row0, cost in q:
+                    if not pairs or pairs[-1] != (r_, g_):
+                        assert (r_, g_) not in totals
+                        pairs.append((r_, g_))
+                    totals[(r_, g_)] = totals.get((r_, g_), 0) + cost
+                for pr in pairs:
+                    cs = [c for r_, g_, _, c in q if (r_, g_) == pr]
+                    assert cs == sorted(cs, reverse=True)
+                tl = [totals[pr] for pr in pairs]
+                assert tl == sorted(tl, reverse=True)
         else:
             costs = [t[3] for t in real]
             assert costs == sorted(costs, reverse=True)
+
+
+@pytest.mark.parametrize("grouped", [False, True])
+def test_plan_writes_exactly_plan_words(grouped):
+    """The plan fills exactly the size cw_suffix_prefill_plan_words reports, with
+    empty requests anywhere in the batch (guard words after the buffer stay intact)."""
+    B = 40 if grouped else 3
+    S = np.array([0, 5, 0, 700, 33, 0] * 7, dtype=np.int32)[:B]
+    P = np.arange(B, dtype=np.int32) % 5 * 16
+    cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
+    cu_a, cu_p = _arr(cu)
+    pl_a, pl_p = _arr(P)
+    words = cw.lib().cw_suffix_prefill_plan_words(cu_p, pl_p, B, 32, 8, 128)
+    assert words > 0
+    buf = np.full(words + 256, -7, dtype=np.int32)
+    n = ctypes.c_int32(0)
+    st = cw.lib().cw_suffix_prefill_plan(cu_p, pl_p, B, 32, 8, 128,
+                                         buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), words,
+                                         ctypes.byref(n))
+    assert st == cw.CW_OK and 4 * n.value == words
+    assert (buf[words:] == -7).all()
+    assert _grouped(buf[:words], n.value, 8) == grouped
+    seen = _plan_rows(buf, n.value, cu, 8, 32)
+    assert len(seen) == int(S.sum()) * 8 and set(seen.values()) == {1}
 
 
 def test_plan_groups_pairs_on_one_partition():
