@@ -575,7 +575,7 @@ cw_status plan_args(const int32_t* cu, const int32_t* plen, int32_t batch, int32
   if (batch < 1) return fail(CW_EINVAL, "batch must be >= 1");
   if (hq < 1 || hkv < 1 || hq % hkv != 0)
     return fail(CW_EINVAL, "num_q_heads must be a positive multiple of num_kv_heads");
-  if (hq / hkv > cw::kTileRows) return fail(CW_EUNSUPPORTED, "more than 128 query heads per KV head");
+  if (hq / hkv > cw::kMaxGroup) return fail(CW_EUNSUPPORTED, "more than 128 query heads per KV head");
   if (d != 64 && d != 128) return fail(CW_EUNSUPPORTED, "head_dim must be 64 or 128");
   if (cu[0] != 0) return fail(CW_EINVAL, "cu_suffix[0] must be 0");
   for (int32_t r = 0; r < batch; ++r) {

@@ -52,26 +52,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // ---------------------------------------------------------------------------
-// KV append: thread u moves 16 bytes; u enumerates (suffix row, K|V, head,
-// 16-byte chunk of D), so reads of k_new/v_new are contiguous per row and
-// writes are contiguous per (row, head).
+// KV append: one workgroup per suffix row. The row's request, position and
+// destination block are found once per workgroup (uniform, scalar); each
+// thread then moves 16-byte chunks, K first then V, so reads of k_new/v_new
+// are contiguous per row and writes are contiguous per (row, head).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(
     const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_cache,
     u32x4* __restrict__ v_cache, const int32_t* __restrict__ bt, int bt_stride,
     const int32_t* __restrict__ cu, const int32_t* __restrict__ plen, int batch, int hkv,
-    int chunks_per_head, int num_blocks, int64_t total_units) {
-  const int64_t u = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-  if (u >= total_units) return;
-  const int per_head = chunks_per_head;
-  const int per_tensor = hkv * per_head;
-  const int per_row = 2 * per_tensor;
-  const int row = int(u / per_row);
-  int rem = int(u - int64_t(row) * per_row);
-  const int tensor = rem >= per_tensor;
-  rem -= tensor * per_tensor;
-  const int h = rem / per_head;
-  const int c = rem - h * per_head;
+    int chunks_per_head, int num_blocks) {
+  const int row = blockIdx.x;
   // request owning this row: the largest r with cu[r] <= row
   int lo = 0, hi = batch;
   while (hi - lo > 1) {
@@ -81,10 +72,18 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
   const int t = plen[lo] + (row - cu[lo]);
   const int blk = bt[int64_t(lo) * bt_stride + t / kBs];
   if (blk < 0 || blk >= num_blocks) return;
-  const int64_t src = int64_t(row) * per_tensor + h * per_head + c;
-  const int64_t dst = ((int64_t(blk) * hkv + h) * kBs + (t % kBs)) * per_head + c;
-  if (tensor) v_cache[dst] = v_new[src];
-  else k_cache[dst] = k_new[src];
+  const int per_tensor = hkv * chunks_per_head;
+  const int64_t src0 = int64_t(row) * per_tensor;
+  const int64_t dst0 = (int64_t(blk) * hkv * kBs + (t % kBs)) * chunks_per_head;
+  for (int c = threadIdx.x; c < 2 * per_tensor; c += kThreads) {
+    const int tensor = c >= per_tensor;
+    const int cc = c - tensor * per_tensor;
+    const int h = cc / chunks_per_head;
+    const int ch = cc - h * chunks_per_head;
+    const int64_t dst = dst0 + int64_t(h) * kBs * chunks_per_head + ch;
+    if (tensor) v_cache[dst] = v_new[src0 + cc];
+    else k_cache[dst] = k_new[src0 + cc];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -382,14 +381,12 @@ extern "C" cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_
   if (st != CW_OK) return st;
   if (rows == 0) return cw::ok();
   const int cph = head_dim / 8;
-  const int64_t units = rows * 2 * num_kv_heads * cph;
-  const int64_t grid = (units + kThreads - 1) / kThreads;
-  if (grid > INT32_MAX) return cw::fail(CW_EUNSUPPORTED, "kv_append: batch too large");
-  hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(grid)), dim3(kThreads), 0,
+  if (rows > INT32_MAX) return cw::fail(CW_EUNSUPPORTED, "kv_append: batch too large");
+  hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(rows)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(k_new),
                      static_cast<const u32x4*>(v_new), static_cast<u32x4*>(k_cache),
                      static_cast<u32x4*>(v_cache), block_table, bt_stride, cu_suffix_dev,
-                     prefix_len_dev, batch, num_kv_heads, cph, num_blocks, units);
+                     prefix_len_dev, batch, num_kv_heads, cph, num_blocks);
   return check_launch("kv_append launch");
 }
 
@@ -412,7 +409,7 @@ extern "C" cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, 
     return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn: head_dim must be 64 or 128");
   if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn: block_size must be 16");
   const int group = num_q_heads / num_kv_heads;
-  if (group > cw::kTileRows)
+  if (group > cw::kMaxGroup)
     return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn: more than 128 query heads per KV head");
   int64_t rows = 0;
   cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &rows);

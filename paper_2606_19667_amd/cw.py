@@ -324,3 +324,132 @@ def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
         k_cache.shape[0], float(softmax_scale), _dev(meta.plan, torch.int32, "plan"), meta.num_tiles,
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
+
+
+# ---------------------------------------------------------------- repeated calls
+class BatchRunner:
+    """Pre-bound calls for running the same kind of batch repeatedly.
+
+    Holds the flattened prompt tokens, host buffers for the block table,
+    offsets and plan (pinned when a GPU is present, so their uploads are
+    asynchronous), the device copies, and the C entry points with their
+    arguments converted once. Each schedule() / upload() / launch call is then
+    one ctypes call on cached arguments; the C library still validates every
+    call.
+    """
+
+    def __init__(self, prompts, bt_stride: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                 block_size: int = BLOCK_SIZE, device="cuda"):
+        toks = [_i32_array(p, "tokens") for p in prompts]
+        self.batch = B = len(toks)
+        self.bt_stride = int(bt_stride)
+        self.block_size = int(block_size)
+        self.num_q_heads, self.num_kv_heads, self.head_dim = num_q_heads, num_kv_heads, head_dim
+        self.tokens = np.ascontiguousarray(np.concatenate(toks), dtype=np.int32)
+        self.cu_tokens = np.zeros(B + 1, dtype=np.int64)
+        self.cu_tokens[1:] = np.cumsum([len(t) for t in toks])
+        pin = torch.cuda.is_available()
+        # worst-case plan size: every request with all its prompt as suffix
+        max_cu = np.zeros(B + 1, dtype=np.int32)
+        max_cu[1:] = np.cumsum(np.diff(self.cu_tokens))
+        zero = np.zeros(B, dtype=np.int32)
+        words = int(_lib.cw_suffix_prefill_plan_words(_ptr(max_cu, ctypes.c_int32), _ptr(zero, ctypes.c_int32),
+                                                      B, num_q_heads, num_kv_heads, head_dim))
+        if words < 0:
+            _check(words)
+        self.plan_capacity = max(words, 4) * 8
+        # One host buffer (pinned when a GPU is present) and one device buffer
+        # hold [block table | cu_suffix | prefix_len | plan], so a step uploads
+        # its schedule with a single asynchronous copy. Sections start on
+        # 16-byte boundaries (the plan is read as 16-byte entries).
+        def up4(n):
+            return (n + 3) // 4 * 4
+        o_bt, o_cu = 0, up4(B * bt_stride)
+        o_pl = o_cu + up4(B + 1)
+        o_plan = o_pl + up4(B)
+        total = o_plan + self.plan_capacity
+        self._host = torch.empty(total, dtype=torch.int32, pin_memory=pin)
+        h = self._host.numpy()
+        self.bt_host = h[o_bt:o_bt + B * bt_stride].reshape(B, bt_stride)
+        self.cu_host = h[o_cu:o_cu + B + 1]
+        self.plen_host = h[o_pl:o_pl + B]
+        self.plan_host = h[o_plan:o_plan + self.plan_capacity]
+        self._o_plan = o_plan
+        self.num_tiles = 0
+        self.device = device
+        self._dev = torch.empty(total, dtype=torch.int32, device=device)
+        self.bt = self._dev[o_bt:o_bt + B * bt_stride].view(B, bt_stride)
+        self.cu = self._dev[o_cu:o_cu + B + 1]
+        self.plen = self._dev[o_pl:o_pl + B]
+        self.plan = self._dev[o_plan:o_plan + self.plan_capacity]
+        self._n = ctypes.c_int32(0)
+        p32 = lambda a: _ptr(a, ctypes.c_int32)
+        self._p = {"tok": p32(self.tokens), "cut": _ptr(self.cu_tokens, ctypes.c_int64), "bt": p32(self.bt_host),
+                   "cu": p32(self.cu_host), "pl": p32(self.plen_host), "plan": p32(self.plan_host)}
+        self._append_args = None
+        self._attn_args = None
+
+    @property
+    def total_rows(self) -> int:
+        return int(self.cu_host[-1])
+
+    def schedule(self, pool: Pool) -> None:
+        """cw_schedule_batch into the host buffers, then the tile plan."""
+        p = self._p
+        _check(_lib.cw_schedule_batch(pool.handle, p["tok"], p["cut"], self.batch, self.block_size, self.bt_stride,
+                                      p["bt"], p["pl"], p["cu"]))
+        _check(_lib.cw_suffix_prefill_plan(p["cu"], p["pl"], self.batch, self.num_q_heads, self.num_kv_heads,
+                                           self.head_dim, p["plan"], self.plan_capacity, ctypes.byref(self._n)))
+        self.num_tiles = self._n.value
+
+    def set_schedule(self, block_table, prefix_len, cu_suffix) -> None:
+        """Use a given schedule instead of cw_schedule_batch (fixed-depth batches)."""
+        self.bt_host[...] = block_table
+        self.plen_host[...] = prefix_len
+        self.cu_host[...] = cu_suffix
+        p = self._p
+        _check(_lib.cw_suffix_prefill_plan(p["cu"], p["pl"], self.batch, self.num_q_heads, self.num_kv_heads,
+                                           self.head_dim, p["plan"], self.plan_capacity, ctypes.byref(self._n)))
+        self.num_tiles = self._n.value
+
+    def release(self, pool: Pool) -> None:
+        p = self._p
+        _check(_lib.cw_release_batch(pool.handle, p["bt"], self.bt_stride, p["pl"], p["cu"], self.batch,
+                                     self.block_size))
+
+    def upload(self) -> None:
+        """One asynchronous copy of the host schedule to the device buffer (current stream)."""
+        n = self._o_plan + 4 * max(self.num_tiles, 1)
+        self._dev[:n].copy_(self._host[:n], non_blocking=True)
+
+    def bind(self, q, k_new, v_new, k_cache, v_cache, out, softmax_scale: float, stream=None) -> None:
+        """Fixes the tensors of the device calls (checked once here)."""
+        hq, hkv, D = self.num_q_heads, self.num_kv_heads, self.head_dim
+        for name, t, dt in (("q", q, torch.bfloat16), ("k_new", k_new, torch.bfloat16),
+                            ("v_new", v_new, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                            ("v_cache", v_cache, torch.bfloat16), ("out", out, torch.bfloat16)):
+            _dev(t, dt, name)
+        if k_cache.dim() != 4 or tuple(k_cache.shape[1:]) != (hkv, BLOCK_SIZE, D) or v_cache.shape != k_cache.shape:
+            raise ValueError("caches must be [num_blocks, Hkv, 16, D]")
+        self._tensors = (q, k_new, v_new, k_cache, v_cache, out)
+        s = _stream(stream)
+        p = self._p
+        self._append_args = [k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                             self.bt.data_ptr(), self.bt_stride, self.cu.data_ptr(), self.plen.data_ptr(),
+                             p["cu"], p["pl"], self.batch, hkv, D, BLOCK_SIZE, k_cache.shape[0], s]
+        self._attn_args = [q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), self.bt.data_ptr(), self.bt_stride,
+                           self.cu.data_ptr(), self.plen.data_ptr(), p["cu"], p["pl"], self.batch, hq, hkv, D,
+                           BLOCK_SIZE, k_cache.shape[0], float(softmax_scale), self.plan.data_ptr(), 0,
+                           out.data_ptr(), s]
+        self._rows = (q.shape[0], k_new.shape[0], v_new.shape[0], out.shape[0])
+
+    def kv_append(self) -> None:
+        if any(n != self.total_rows for n in self._rows):
+            raise ValueError("bound tensors do not match the scheduled suffix rows")
+        _check(_lib.cw_kv_append(*self._append_args))
+
+    def attention(self) -> None:
+        if any(n != self.total_rows for n in self._rows):
+            raise ValueError("bound tensors do not match the scheduled suffix rows")
+        self._attn_args[17] = self.num_tiles
+        _check(_lib.cw_suffix_prefill_attn(*self._attn_args))

@@ -221,3 +221,31 @@ def test_long_context_70b_sampled(hit):
     _compare_sampled(db, _run(db), [0, w.batch - 1])
     del db
     _cleanup()
+
+
+def test_prebound_runner_matches_binding_path_bitwise():
+    """The pre-bound path the bench times (one schedule call, one packed upload,
+    cached launch arguments) computes exactly what the plain binding computes."""
+    w = W.llama8b_trace_batch(seed=4, batch=6, warmup=20)
+    db = B.materialize(w, keep_host=[])
+    ref = _run(db)
+    stride = B.bt_stride_for(w)
+    pool = cw.Pool(w.num_blocks(), w.free_order())
+    for p in w.warmup:
+        bt, pl, cu = cw.schedule_batch(pool, [p.tokens(w.seed)], stride)
+        cw.release_batch(pool, bt, pl, cu)
+    rn = cw.BatchRunner([p.tokens(w.seed) for p in w.prompts], stride, w.num_q_heads, w.num_kv_heads,
+                        w.head_dim)
+    rn.schedule(pool)
+    assert np.array_equal(rn.bt_host, db.sched.block_table) and np.array_equal(rn.plen_host, db.sched.prefix_len)
+    out = torch.empty_like(db.q)
+    k2, v2 = db.k_cache.clone(), db.v_cache.clone()
+    rn.bind(db.q, db.k_new, db.v_new, k2, v2, out, w.scale)
+    rn.upload()
+    rn.kv_append()
+    rn.attention()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    assert torch.equal(k2.view(torch.int16), db.k_cache.view(torch.int16))
+    rn.release(pool)
+    _cleanup()
