@@ -24,8 +24,9 @@
  *  - Layouts (all row-major, bf16 = IEEE bfloat16 bit patterns):
  *      q, out        [total_s, Hq, D]        suffix rows of all requests, request-major
  *      k_new, v_new  [total_s, Hkv, D]
- *      k_cache,
- *      v_cache       [num_blocks, Hkv, block_size, D]
+ *      k_cache       [num_blocks, Hkv, block_size, D]   block rows are tokens
+ *      v_cache       [num_blocks, Hkv, D, block_size]   each block transposed: rows are
+ *                    head dimensions, so 16 bytes hold 8 consecutive tokens of one d
  *      block_table   int32 [batch, bt_stride]; row r lists the physical blocks of
  *                    request r's logical blocks 0 .. ceil(L_r / block_size) - 1
  *      cu_suffix     int32 [batch + 1]; request r owns rows cu[r] .. cu[r+1]-1,
@@ -53,7 +54,7 @@ typedef int32_t cw_status;
 #define CW_ENOSPC (-3)       /* block pool exhausted */
 #define CW_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
 
-#define CW_ABI_VERSION 1
+#define CW_ABI_VERSION 2
 
 /* ABI version of the loaded library (CW_ABI_VERSION at build time). */
 int32_t cw_abi_version(void);
@@ -166,7 +167,8 @@ cw_status cw_release_batch(cw_pool* pool, const int32_t* block_table, int32_t bt
  *
  * For every request r and token t in [P_r, L_r):
  *   k_cache[block_table[r, t / bs], h, t % bs, :] = k_new[cu[r] + t - P_r, h, :]
- * and the same for V; a bit copy. Nothing else in the caches changes. A block
+ *   v_cache[block_table[r, t / bs], h, :, t % bs] = v_new[cu[r] + t - P_r, h, :]
+ * a bit copy. Nothing else in the caches changes. A block
  * ID outside [0, num_blocks) drops the write (never faults).
  *   cu_suffix_dev / prefix_len_dev   device copies read by the kernel
  *   cu_suffix_host / prefix_len_host host copies used for validation and
@@ -185,8 +187,9 @@ cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_cache, void
 /* ------------------------------------------------------------------------
  * Host: tile schedule for cw_suffix_prefill_attn.
  *
- * The attention kernel works on tiles of (request, KV head, run of suffix
- * rows); the plan lists them heaviest first and groups the tiles of one
+ * The attention kernel works on tiles of (request, KV head, run of
+ * 256 / (Hq / Hkv) suffix rows), i.e. 256 packed (query head, row) pairs;
+ * the plan lists them heaviest first and groups the tiles of one
  * (request, KV head) on one L2 partition. A plan depends only on the batch
  * shape, so one plan serves every layer of a model for that batch.
  *

@@ -194,14 +194,23 @@ class PoolSim:
                 self.free.append(b)
 
 
-def kv_append_image(cache, new, block_table, cu_suffix, prefix_len, block_size: int = 16):
+def kv_append_image(cache, new, block_table, cu_suffix, prefix_len, block_size: int = 16,
+                    layout: str = "slot_d"):
     """Expected cache after writing each request's suffix K (or V) into its blocks.
 
-    cache: [NB, Hkv, bs, D] array (any dtype; bits are copied, never converted);
-    new: [total_s, Hkv, D]; block_table: [B, stride] int; cu_suffix: [B + 1];
-    prefix_len: [B]. Token t of request r (P_r <= t < P_r + S_r) lands in block
-    block_table[r, t // bs] at slot t % bs; every other element keeps its value.
+    Paper Sec. 2.1: the K/V of a prompt live in fixed-size blocks named by a
+    per-request block table; after the prefix match only the suffix tokens'
+    K/V are computed and written. Token t of request r (P_r <= t < P_r + S_r)
+    lands in block block_table[r, t // bs] at slot t % bs; every other
+    element keeps its value.
+
+    layout "slot_d": cache is [NB, Hkv, bs, D] (the K cache);
+    layout "d_slot": cache is [NB, Hkv, D, bs], each block stored transposed
+    (the V cache). new: [total_s, Hkv, D]; block_table: [B, stride] int;
+    cu_suffix: [B + 1]; prefix_len: [B]. Bits are copied, never converted.
     """
+    if layout not in ("slot_d", "d_slot"):
+        raise ValueError(f"unknown layout {layout!r}")
     out = np.array(cache, copy=True)
     new = np.asarray(new)
     bt = np.asarray(block_table)
@@ -211,13 +220,19 @@ def kv_append_image(cache, new, block_table, cu_suffix, prefix_len, block_size: 
         t = np.arange(p, p + s)
         blocks = bt[r, t // block_size]
         slots = t % block_size
-        out[blocks, :, slots, :] = new[int(cu_suffix[r]) + (t - p)]
+        rows = new[int(cu_suffix[r]) + (t - p)]          # [s, Hkv, D]
+        if layout == "slot_d":
+            out[blocks, :, slots, :] = rows
+        else:
+            out[blocks, :, :, slots] = rows
     return out
 
 
-def kv_append_image_loops(cache, new, block_table, cu_suffix, prefix_len, block_size: int = 16):
-    """The same scatter as `kv_append_image`, one token and head at a time."""
+def kv_append_image_loops(cache, new, block_table, cu_suffix, prefix_len, block_size: int = 16,
+                          layout: str = "slot_d"):
+    """The same scatter as `kv_append_image`, one element at a time."""
     out = np.array(cache, copy=True)
+    D = np.asarray(new).shape[2]
     for r in range(len(prefix_len)):
         p = int(prefix_len[r])
         s = int(cu_suffix[r + 1]) - int(cu_suffix[r])
@@ -225,5 +240,10 @@ def kv_append_image_loops(cache, new, block_table, cu_suffix, prefix_len, block_
             t = p + i
             blk = int(block_table[r][t // block_size])
             for g in range(out.shape[1]):
-                out[blk, g, t % block_size, :] = new[int(cu_suffix[r]) + i, g, :]
+                for d in range(D):
+                    val = new[int(cu_suffix[r]) + i, g, d]
+                    if layout == "slot_d":
+                        out[blk, g, t % block_size, d] = val
+                    else:
+                        out[blk, g, d, t % block_size] = val
     return out

@@ -15,7 +15,7 @@ cw_status ok();
 
 // Tile geometry of the attention kernel, shared with the planner.
 constexpr int kBlockSize = 16;   // tokens per KV block
-constexpr int kTileRows = 128;   // packed query rows (heads x positions) per workgroup
+constexpr int kTileRows = 256;   // packed query rows (heads x positions) per workgroup
 constexpr int kKvTile = 64;      // keys staged in LDS per step
 constexpr int kNumXcd = 8;       // L2 partitions; workgroup i runs on partition i % 8
 constexpr int kMaxGroup = 128;   // query heads per KV head supported

@@ -52,78 +52,196 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // ---------------------------------------------------------------------------
-// KV append: one workgroup per suffix row. The row's request, position and
-// destination block are found once per workgroup (uniform, scalar); each
-// thread then moves 16-byte chunks, K first then V, so reads of k_new/v_new
-// are contiguous per row and writes are contiguous per (row, head).
+// KV append. The unit of work is one block of suffix rows: request r
+// contributes ceil(S_r / 16) units, unit j covering suffix rows 16 j ..
+// min(16 j + 16, S_r) - 1, which (P_r being a multiple of 16) fill slots
+// 0 .. of a single cache block. One workgroup per unit finds its (request,
+// unit) with a wave-wide prefix sum over the per-request unit counts, copies
+// the K rows ([slot][d] in the cache, contiguous 16-byte chunks) and writes V
+// transposed ([d][slot]) through LDS, 16-byte stores per 8-slot half row for
+// a full block and one element per slot for a partial one.
 // ---------------------------------------------------------------------------
+constexpr int kAppendLds = 32768;   // bytes of V rows staged per pass
+
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(
     const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_cache,
-    u32x4* __restrict__ v_cache, const int32_t* __restrict__ bt, int bt_stride,
-    const int32_t* __restrict__ cu, const int32_t* __restrict__ plen, int batch, int hkv,
-    int chunks_per_head, int num_blocks) {
-  const int row = blockIdx.x;
-  // request owning this row: the largest r with cu[r] <= row
-  int lo = 0, hi = batch;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (cu[mid] <= row) lo = mid; else hi = mid;
+    uint16_t* __restrict__ v_cache, const int32_t* __restrict__ bt, int bt_stride,
+    const int32_t* __restrict__ cu, const int32_t* __restrict__ plen, int batch, int hkv, int D,
+    int num_blocks) {
+  __shared__ int s_unit[2];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[kAppendLds / 2];
+  const int tid = threadIdx.x;
+  if (tid < 64) {
+    const int b = blockIdx.x;
+    int base = 0, rr = -1, jb = 0;
+    for (int r0 = 0; r0 < batch; r0 += 64) {
+      const int r = r0 + tid;
+      const int n = r < batch ? (cu[r + 1] - cu[r] + kBs - 1) / kBs : 0;
+      int x = n;   // inclusive prefix sum of n over the lanes
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (tid >= off) x += y;
+      }
+      const uint64_t hit = __ballot(base + x - n <= b && b < base + x);
+      if (hit) {
+        const int l = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+        rr = r0 + l;
+        jb = b - base - __shfl(x - n, l);
+        break;
+      }
+      base += __shfl(x, 63);
+    }
+    if (tid == 0) {
+      s_unit[0] = rr;
+      s_unit[1] = jb;
+    }
   }
-  const int t = plen[lo] + (row - cu[lo]);
-  const int blk = bt[int64_t(lo) * bt_stride + t / kBs];
-  if (blk < 0 || blk >= num_blocks) return;
-  const int per_tensor = hkv * chunks_per_head;
-  const int64_t src0 = int64_t(row) * per_tensor;
-  const int64_t dst0 = (int64_t(blk) * hkv * kBs + (t % kBs)) * chunks_per_head;
-  for (int c = threadIdx.x; c < 2 * per_tensor; c += kThreads) {
-    const int tensor = c >= per_tensor;
-    const int cc = c - tensor * per_tensor;
-    const int h = cc / chunks_per_head;
-    const int ch = cc - h * chunks_per_head;
-    const int64_t dst = dst0 + int64_t(h) * kBs * chunks_per_head + ch;
-    if (tensor) v_cache[dst] = v_new[src0 + cc];
-    else k_cache[dst] = k_new[src0 + cc];
+  __syncthreads();
+  const int r = s_unit[0];
+  if (r < 0) return;
+  const int j0 = kBs * s_unit[1];
+  const int cu0 = cu[r];
+  const int nv = min(kBs, cu[r + 1] - cu0 - j0);
+  const int t0 = plen[r] + j0;
+  const int blk = bt[int64_t(r) * bt_stride + t0 / kBs];
+  if (nv <= 0 || blk < 0 || blk >= num_blocks) return;
+
+  const int nch = D / 8;   // 16-byte chunks per row and head
+  const int64_t src0 = int64_t(cu0 + j0) * hkv * nch;
+  // K: source chunk c = (slot, head, chunk) -> cache [blk][head][slot][chunk]
+  u32x4* kd = k_cache + int64_t(blk) * hkv * kBs * nch;
+  for (int c = tid; c < nv * hkv * nch; c += kThreads) {
+    const int ch = c & (nch - 1);
+    const int rest = c / nch;
+    const int h = rest % hkv;
+    const int slot = rest / hkv;
+    kd[(h * kBs + slot) * nch + ch] = k_new[src0 + c];
+  }
+  // V: stage [head][slot][d] in LDS, then write [blk][head][d][slot].
+  const int hc = max(1, kAppendLds / (kBs * D * 2));
+  uint16_t* vd = v_cache + int64_t(blk) * hkv * D * kBs;
+  for (int h0 = 0; h0 < hkv; h0 += hc) {
+    const int nh = min(hc, hkv - h0);
+    for (int c = tid; c < nv * nh * nch; c += kThreads) {
+      const int ch = c & (nch - 1);
+      const int rest = c / nch;
+      const int hl = rest % nh;
+      const int slot = rest / nh;
+      reinterpret_cast<u32x4*>(tile)[(hl * kBs + slot) * nch + ch] =
+          v_new[src0 + (int64_t(slot) * hkv + h0 + hl) * nch + ch];
+    }
+    __syncthreads();
+    for (int u = tid; u < nh * D * 2; u += kThreads) {
+      const int part = u & 1;
+      const int d = (u >> 1) & (D - 1);
+      const int hl = (u >> 1) / D;
+      const uint16_t* src = tile + (hl * kBs + 8 * part) * D + d;
+      uint16_t* dst = vd + (int64_t(h0 + hl) * D + d) * kBs + 8 * part;
+      if (nv == kBs) {
+        u32x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = uint32_t(src[2 * j * D]) | (uint32_t(src[(2 * j + 1) * D]) << 16);
+        *reinterpret_cast<u32x4*>(dst) = w;
+      } else {
+        for (int j = 0; j < 8 && 8 * part + j < nv; ++j) dst[j] = src[j * D];
+      }
+    }
+    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
 // Suffix prefill attention.
 //
-// LDS holds two K/V stages (double buffering, one barrier per 64-key step).
-// The next step's K/V are fetched into registers while the current step is
-// computed, then written into the other stage.
-//  * K: row-major [key][d], rows padded by 16 bytes, so the 16-row groups of
-//    the QK^T operand reads fall on distinct banks.
-//  * V: row-major [key][d] with the 16-byte chunks of each row XOR-swizzled by
-//    fv(row), spreading the eight rows one transposing read touches over all
-//    chunk groups. V feeds the PV MFMA through ds_read_b64_tr_b16: in each
-//    16-lane group, lane o receives element o % 4 of the 8-byte pieces addressed
-//    by lanes o / 4 + 4 j, j = 0..3; so lane i addresses key (base + i / 4),
-//    d (base + 4 (i % 4)), and lane o receives d = base + o for four keys.
+// Work split: one workgroup = 8 wavefronts (two per SIMD) = one tile of 256
+// packed query rows; wave w owns query columns 32 w .. 32 w + 31 and walks the
+// tile's keys in steps of 64.
+//
+// Per wave the step loop is software-pipelined so that matrix and vector work
+// of different steps overlap inside one instruction stream:
+//   step j:  S(j+1) = K(j+1) Q^T  (16 MFMAs)  ||  P(j) = exp2(S(j))  (VALU)
+//            O^T += V(j)^T P(j)^T (16 MFMAs)  ||  mask + row max of S(j+1)
+//
+// K/V staging: LDS holds three stages of (K, V) for one 64-key step. The
+// cache blocks are copied into LDS by the LDS-direct loads (global_load_lds),
+// which need no registers: wave w moves K (w even) or V (w odd) of block w / 2
+// of a step, K three steps and V two steps ahead of their use, and waits for
+// its copies of the step after next only at the end of the following step, so
+// each copy has two steps to land. A block that is missing or reaches past the
+// prompt end goes through registers instead and is zero-filled, so stale cache
+// bytes never meet a zero probability. One barrier ends each step.
+//
+// Softmax in base 2 with lazy rescaling. Q is pre-multiplied by
+// softmax_scale * log2(e) (rounded to bf16), and each S accumulator starts
+// from -m, the running exponent base, so the MFMA result is already the
+// exponent s - m. The base moves only when a row's step maximum exceeds it by
+// more than 8 (a factor 256), and then O and l are rescaled once; probabilities
+// therefore stay below 256 and the fp32 sums cannot overflow.
+//
+// LDS layouts (per stage). A load-to-LDS instruction writes 64 x 16 bytes
+// contiguously in lane order, so swizzles are applied on the global side
+// (each lane fetches the 16 bytes that belong at its LDS slot).
+//  * K: row-major [key][d] (RB bytes per row); 16-byte chunk c of row r is
+//    stored at c ^ kswz(r), which puts the 16 rows of every operand read phase
+//    on distinct banks.
+//  * V: the cache holds each block transposed, [d][slot]; LDS keeps that per
+//    block ([block][d][16 keys], 32-byte rows) with the two 16-byte halves of
+//    row d swapped when bit 3 of d is set (conflict-free operand reads).
+//  * Key order: the PV MFMA's B operand is the score accumulator itself. In
+//    the 32x32 accumulator, lane half u, register e holds row
+//    8 (e / 4) + 4 u + e % 4. Reading K row pi(i) into A row i, with pi
+//    swapping bits 2 and 3 of i, makes that register hold key
+//    16 (e / 8) + 8 u + e % 8 (plus 32 per 32-key half), so for the 16-key
+//    slice kk of the PV product lane half u holds keys 16 kk + 8 u .. + 7 in
+//    order: block kk, half u of a V^T row, one 16-byte read.
 // ---------------------------------------------------------------------------
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
-typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l. (Kept
+// out of the kernel template: the host pass of a template that names this
+// builtin directly emits no launch stub.)
+__device__ __forceinline__ void copy16_to_lds(const void* src, lds_void_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+constexpr int kAttnWaves = 8;
+constexpr int kAttnThreads = 64 * kAttnWaves;
+static_assert(kAttnWaves * 32 == cw::kTileRows, "one 32-column MFMA block per wave");
+constexpr int kStages = 3;
 
 template <int D>
 struct AttnGeom {
-  static constexpr int RB = 2 * D;              // bytes per K/V row in global memory
-  static constexpr int KRB = RB + 16;           // padded K row in LDS
-  static constexpr int NC = D / 8;              // 16-byte chunks per row
-  static constexpr int KTILE = kKv * KRB;
-  static constexpr int VTILE = kKv * RB;
+  static constexpr int RB = 2 * D;              // bytes per K row
+  static constexpr int NC = D / 8;              // 16-byte chunks per K row
+  static constexpr int KTILE = kKv * RB;        // K of one step
+  static constexpr int BLK = D * 2 * kBs;       // one V^T block (D rows of 16 keys)
+  static constexpr int VTILE = (kKv / kBs) * BLK;
   static constexpr int STAGE = KTILE + VTILE;
-  static constexpr int RPL = 1024 / RB;         // rows covered by one wave-wide 16-byte load
-  static constexpr int LPW = kBs / RPL;         // loads per wave per tensor (one block)
+  static constexpr int RPL = 1024 / RB;         // K rows per 1 KB copy
+  static constexpr int LPW = kBs * RB / 1024;   // 1 KB copies per block and tensor
   static constexpr int KS = D / 16;             // MFMA k-steps over D
   static constexpr int DT = D / 32;             // 32-row output tiles over D
-  __device__ static int vswz(int row) {
-    return D == 128 ? (4 * (row & 3) + ((row >> 2) & 3)) : (row & (NC - 1));
-  }
+  // chunk swizzle of K row r (rows of 256 bytes: 16 chunks; of 128 bytes: 8)
+  __device__ static int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 };
 
+constexpr float kLazy = 8.0f;   // rescale when a score exceeds the base by 2^8
+
+// s_waitcnt immediates (gfx9 encoding): vmcnt(n) with lgkmcnt(0), expcnt untouched.
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | (7 << 4) | ((n >> 4) << 14); }
+
+// x * c rounded to bfloat16, for the 8 bfloat16 values of one Q fragment.
+__device__ __forceinline__ bf16x8 scale_bf16x8(u32x4 raw, float c) {
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    o[j] = pack_bf16x2(__uint_as_float(raw[j] << 16) * c, __uint_as_float(raw[j] & 0xFFFF0000u) * c);
+  return __builtin_bit_cast(bf16x8, u32x4{o[0], o[1], o[2], o[3]});
+}
+
 template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
                                 const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
                                 int bt_stride, const int32_t* __restrict__ cu,
@@ -131,8 +249,9 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
                                 int batch, int hq, int hkv, int group, int per_tile, int num_blocks,
                                 float c_log2, uint16_t* __restrict__ out) {
   using G = AttnGeom<D>;
-  constexpr int KS = G::KS, DT = G::DT, RB = G::RB, KRB = G::KRB, NC = G::NC, LPW = G::LPW;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * G::STAGE];
+  constexpr int KS = G::KS, DT = G::DT, RB = G::RB, NC = G::NC, LPW = G::LPW, RPL = G::RPL;
+  constexpr int KTILE = G::KTILE, BLK = G::BLK, STAGE = G::STAGE;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE];
 
   const int4 item = plan[blockIdx.x];
   const int r = item.x, g = item.y, row0 = item.z;
@@ -145,6 +264,8 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   const int nvalid = min(per_tile, S - row0);
   const int kv_end = P + row0 + nvalid;
   const int ntiles = (kv_end + kKv - 1) / kKv;
+  // steps 0 .. n_full - 1 are visible to every row of the tile (no mask)
+  const int n_full = min(ntiles, (P + row0 + 1) / kKv);
   const int nblk = (L + kBs - 1) / kBs;
   const int32_t* btr = bt + int64_t(r) * bt_stride;
 
@@ -167,177 +288,241 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   if (row_ok) {
     const u32x4* qp = reinterpret_cast<const u32x4*>(q + (qrow * hq + head) * D);
 #pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, qp[2 * s + half]);
+    for (int s = 0; s < KS; ++s) qf[s] = scale_bf16x8(qp[2 * s + half], c_log2);
   } else {
 #pragma unroll
     for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
   }
 
-  // ---- K/V staging. Wave w fetches block w of each 64-key step: LPW 16-byte
-  // loads per tensor per lane, lane l of load i reading row RPL i + l / NC,
-  // chunk l % NC (one contiguous 1 KB run per load).
+  // ---- staging role of this wave: tensor (K or V) of block slot bs of a step
+  const int bs = wave >> 1;
+  const bool is_v = (wave & 1) != 0;
+  const int ahead = is_v ? 2 : 3;   // step j copies the step j + ahead
+  const uint16_t* const cache = is_v ? vc : kc;
+  // Per-lane source offset inside a block (bytes) and LDS destination inside a
+  // stage of copy i (the destination of lane l is dst + 16 l).
+  int src_off[LPW];
+#pragma unroll
+  for (int i = 0; i < LPW; ++i) {
+    if (is_v) {
+      const int d = 32 * i + (lane >> 1);
+      src_off[i] = d * 32 + (((lane & 1) ^ ((lane >> 4) & 1)) << 4);
+    } else {
+      const int row = RPL * i + lane / NC;   // row inside the block
+      src_off[i] = row * RB + (((lane % NC) ^ G::kswz(row)) << 4);
+    }
+  }
+  const int dst0 = is_v ? KTILE + bs * BLK : bs * kBs * RB;
   // Physical block of logical block lb, or -1 past the prompt / outside the
   // pool; the table index is clamped into the request's row (always in bounds).
-  auto block_id = [&](int lb) -> int {
+  auto block_id = [&](int lb) __attribute__((always_inline)) -> int {
     const int b = btr[min(lb, nblk - 1)];
     return (lb < nblk && b >= 0 && b < num_blocks) ? b : -1;
   };
-  const int ld_row = lane / NC;
-  const int ld_ch = lane % NC;
-  u32x4 kreg[LPW], vreg[LPW];
-  auto fetch = [&](int b) {
-    const int bb = b < 0 ? 0 : b;   // block 0 stands in for a missing block; zeroed when staged
-    const uint8_t* kb = reinterpret_cast<const uint8_t*>(kc) + (int64_t(bb) * hkv + g) * (kBs * RB);
-    const uint8_t* vb = reinterpret_cast<const uint8_t*>(vc) + (int64_t(bb) * hkv + g) * (kBs * RB);
-    const int off = ld_row * RB + ld_ch * 16;
-#pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-      kreg[i] = *reinterpret_cast<const u32x4*>(kb + off + i * 1024);
-      vreg[i] = *reinterpret_cast<const u32x4*>(vb + off + i * 1024);
-    }
-  };
-  // Rows of a missing block and rows past the prompt end are written as zeros
-  // (stale cache bytes must never meet a zero probability).
-  auto stage_write = [&](uint8_t* st, int k0, int b) {
-    const int key0 = k0 + kBs * wave;
+  // Stages step t's block of this wave into stage st; returns whether it used
+  // the load-to-LDS path (whose completion the caller then waits for).
+  auto stage_block = [&](int t, int b, int st) __attribute__((always_inline)) -> bool {
+    const int key0 = t * kKv + bs * kBs;
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(cache) +
+                         (int64_t(b < 0 ? 0 : b) * hkv + g) * (kBs * RB);
+    uint8_t* dst = lds + st * STAGE + dst0;
     if (b >= 0 && key0 + kBs <= L) {   // wave-uniform: the whole block is valid
 #pragma unroll
-      for (int i = 0; i < LPW; ++i) {
-        const int row = kBs * wave + G::RPL * i + ld_row;
-        *reinterpret_cast<u32x4*>(st + row * KRB + ld_ch * 16) = kreg[i];
-        *reinterpret_cast<u32x4*>(st + G::KTILE + row * RB + ((ld_ch ^ G::vswz(row)) << 4)) = vreg[i];
-      }
-      return;
+      for (int i = 0; i < LPW; ++i)
+        copy16_to_lds(src + src_off[i], (lds_void_t*)(dst + i * 1024));
+      return true;
     }
     const u32x4 zero{0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < LPW; ++i) {
-      const int row = kBs * wave + G::RPL * i + ld_row;
-      const bool ok = b >= 0 && key0 + G::RPL * i + ld_row < L;
-      *reinterpret_cast<u32x4*>(st + row * KRB + ld_ch * 16) = ok ? kreg[i] : zero;
-      *reinterpret_cast<u32x4*>(st + G::KTILE + row * RB + ((ld_ch ^ G::vswz(row)) << 4)) = ok ? vreg[i] : zero;
+      u32x4 v = b >= 0 ? *reinterpret_cast<const u32x4*>(src + src_off[i]) : zero;
+      if (is_v) {
+        // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
+        const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
+        const int vn = b < 0 ? 0 : min(8, max(0, L - key0 - h8));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
+      } else {
+        const bool ok = b >= 0 && key0 + RPL * i + lane / NC < L;
+        v = ok ? v : zero;
+      }
+      *reinterpret_cast<u32x4*>(dst + i * 1024 + lane * 16) = v;
     }
+    return false;
+  };
+  // End of a step: this wave's copies for the next step have landed (the LPW
+  // copies issued in this step may still be in flight, when `keep` says that
+  // nothing else went to memory after them), LDS writes are done, then the
+  // workgroup barrier. The empty asm statements keep the compiler from moving
+  // memory accesses across the barrier.
+  auto step_barrier = [&](bool keep) __attribute__((always_inline)) {
+    if (keep) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(LPW));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
 
   // ---- per-lane LDS read offsets (relative to a stage)
-  // K operand: row st*32 + l32, chunk 2s + half.
-  const int k_off = l32 * KRB + half * 16;
-  // V operand (transposing read): group gi = lane / 16, i = lane % 16:
-  //   key = 16 kk + 8 sel + 4 (gi / 2) + i / 4,  d = 32 t + 16 (gi % 2) + 4 (i % 4).
-  // vswz(key) depends on key mod 16 only, so kk enters as a constant offset.
-  const int gi = lane >> 4, li = lane & 15;
-  const int vkey_l = 4 * (gi >> 1) + (li >> 2);
-  const int vd_l = 16 * (gi & 1) + 4 * (li & 3);
-  int v_off[DT][2];
+  // K operand: row 32 h + pi(l32), logical chunk 2 s + half.
+  const int k_row = (l32 & ~12) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
+  int k_off[KS];
 #pragma unroll
-  for (int t = 0; t < DT; ++t)
-#pragma unroll
-    for (int sel = 0; sel < 2; ++sel) {
-      const int key = 8 * sel + vkey_l;
-      const int d = 32 * t + vd_l;
-      v_off[t][sel] = G::KTILE + key * RB + (((d >> 3) ^ G::vswz(key)) << 4) + ((d & 4) << 1);
-    }
+  for (int s = 0; s < KS; ++s) k_off[s] = k_row * RB + (((2 * s + half) ^ G::kswz(k_row)) << 4);
+  // V operand: block kk, row d = 32 t + l32, logical half = half.
+  const int v_off = KTILE + l32 * 32 + ((half ^ ((l32 >> 3) & 1)) << 4);
 
-  f32x16 oacc[DT];
-#pragma unroll
-  for (int t = 0; t < DT; ++t) oacc[t] = f32x16{};
-  float m_run = -INFINITY;   // running max (raw score units) used for the exponent
-  float l_run = 0.f;         // this lane's partial row sum (its 32 keys per step)
-  const bf16x2 ones{(__bf16)1.0f, (__bf16)1.0f};
-  // Lazy rescaling: the exponent base m_run moves only when a score exceeds it
-  // by more than 2^8 in probability, so O and l are rarely rescaled.
-  const float lazy = 8.0f / c_log2;
-
-  auto compute = [&](const uint8_t* st, int k0) {
-    // S^T = K Q^T for keys k0 .. k0 + 63 (two 32-key halves).
-    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+  // ---- the four pieces of a step
+  // S^T = K Q^T for one stage, accumulators starting from c0.
+  auto qk = [&](const uint8_t* st, const f32x16& c0, f32x16 (&sc)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < KS; ++s)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(st + k_off + h * 32 * KRB + s * 32));
-        sacc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[h], 0, 0, 0);
+            bf16x8, *reinterpret_cast<const u32x4*>(st + k_off[s] + h * 32 * RB));
+        sc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], s == 0 ? c0 : sc[h], 0, 0, 0);
       }
-    // Causal mask, only where the step reaches past the first row's limit.
-    if (k0 + kKv - 1 > P + row0) {
-      const int lim = qpos - k0;
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = h * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-          if (key > lim) sacc[h][e] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
+  };
+  // Causal mask of the step starting at key k0.
+  auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
+    const int lim = qpos - k0;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[h][e], sacc[h][e + 1]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // key 0 is visible to every row, so after the first step m_run is finite
-    const bool grow = !(mx <= m_run + lazy);
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float m_new = grow ? fmaxf(mx, m_run) : m_run;
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c_log2);
-      l_run *= alpha;
+      for (int e = 0; e < 16; ++e) {
+        const int key = h * 32 + (e >> 3) * 16 + half * 8 + (e & 7);
+        if (key > lim) sc[h][e] = -INFINITY;
+      }
+  };
+  // Maximum of the row over the step's 64 keys (this lane's 32 and lane ^ 32's).
+  auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) -> float {
+    float a = fmaxf(fmaxf(sc[0][0], sc[0][1]), sc[0][2]);
+    float b = fmaxf(fmaxf(sc[1][0], sc[1][1]), sc[1][2]);
 #pragma unroll
-      for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
-      m_run = m_new;
+    for (int e = 3; e < 15; e += 2) {
+      a = fmaxf(fmaxf(a, sc[0][e]), sc[0][e + 1]);
+      b = fmaxf(fmaxf(b, sc[1][e]), sc[1][e + 1]);
     }
-    const float mc = m_run * c_log2;
-    bf16x8 pb[4];
+    a = fmaxf(fmaxf(a, sc[0][15]), sc[1][15]);
+    a = fmaxf(a, b);
+    return fmaxf(a, __shfl_xor(a, 32));
+  };
+  float l_run = 0.f;   // this lane's partial row sum (its 32 keys per step)
+  const bf16x2 ones{(__bf16)1.0f, (__bf16)1.0f};
+  // Probabilities 2^(s - m) as the PV B operand; adds their sum to l_run.
+  auto probs = [&](const f32x16 (&sc)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+    float ls[2] = {0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const int h = kk >> 1, e0 = (kk & 1) * 8;
-      uint32_t w[4];
+      uint32_t w[4];   // a scalar array: bit casts of ext-vector elements are not used
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[h][e0 + 2 * j], c_log2, -mc));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[h][e0 + 2 * j + 1], c_log2, -mc));
-        w[j] = pack_bf16x2(p0, p1);
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[j]), ones, l_run, false);
+        w[j] = pack_bf16x2(__builtin_amdgcn_exp2f(sc[h][e0 + 2 * j]),
+                           __builtin_amdgcn_exp2f(sc[h][e0 + 2 * j + 1]));
+        ls[kk & 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[j]), ones, ls[kk & 1], false);
       }
       pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
-    // O^T += V^T P^T
+    l_run += ls[0] + ls[1];
+  };
+  f32x16 oacc[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t) oacc[t] = f32x16{};
+  // O^T += V^T P^T for one stage.
+  auto pv = [&](const uint8_t* st, const bf16x8 (&pb)[4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const i16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4_t*)((lds_u8_t*)st + v_off[t][0] + kk * 16 * RB));
-        const i16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_i16x4_t*)((lds_u8_t*)st + v_off[t][1] + kk * 16 * RB));
-        const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+        const bf16x8 a = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(st + v_off + kk * BLK + t * 1024));
         oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], oacc[t], 0, 0, 0);
       }
   };
 
-  // One step: fetch the next step's K/V into registers, compute this step from
-  // stage SI, write the registers into the other stage, then one barrier.
-  int b_next = block_id(wave);
-  fetch(b_next);
-  stage_write(lds, 0, b_next);
-  if (ntiles > 1) b_next = block_id(kKv / kBs + wave);
-  __syncthreads();
-  auto step = [&](auto si, int it) {
-    constexpr int SI = decltype(si)::value;
-    const int k0 = it * kKv;
-    const bool more = it + 1 < ntiles;
-    const int b = b_next;
-    if (more) {
-      fetch(b);
-      if (it + 2 < ntiles) b_next = block_id((k0 + 2 * kKv) / kBs + wave);
+  // ---- prologue: stage steps 0 and 1 (and K of step 2); S(0) with the exact
+  // row maximum as base
+  {
+    const int n0 = min(ntiles, ahead);
+    for (int t = 0; t < n0; ++t) stage_block(t, block_id(t * (kKv / kBs) + bs), t);
+  }
+  int bnext = ahead < ntiles ? block_id(ahead * (kKv / kBs) + bs) : -1;   // block copied in step 0
+  step_barrier(false);
+  f32x16 sa[2], sb[2];
+  qk(lds, f32x16{}, sa);
+  if (n_full == 0) mask(sa, 0);
+  f32x16 mneg;   // -m in every element: the start of each S accumulator
+  {
+    const float m0 = rowmax(sa);   // finite: key 0 is visible to every row
+#pragma unroll
+    for (int h = 0; h < 2; ++h) sa[h] -= m0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mneg[e] = -m0;
+  }
+  float mx = 0.f;   // row maximum of the current S (relative to the base)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();   // K of stage 0 is refilled during step 0
+  asm volatile("" ::: "memory");
+
+  // Moves the base up by the step maximum when it exceeds the base by kLazy.
+  auto rebase = [&](f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    const bool grow = mx > kLazy;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float delta = grow ? mx : 0.f;
+      const float alpha = __builtin_amdgcn_exp2f(-delta);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) sc[h] -= delta;
+      mneg -= delta;
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
     }
-    compute(lds + SI * G::STAGE, k0);
-    if (more) stage_write(lds + (1 - SI) * G::STAGE, k0 + kKv, b);
-    __syncthreads();
   };
-  for (int it = 0; it < ntiles; it += 2) {
-    step(std::integral_constant<int, 0>{}, it);
-    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
+  // Step j < ntiles - 1: current S in sc, next S into sn. Stage of step t is
+  // t % 3; this wave copies step j + ahead into stage (j + ahead) % 3.
+  auto step = [&](auto maskc, int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(maskc)::value;
+    rebase(sc);
+    const int tc = j + ahead;
+    bool issued = false;
+    if (tc < ntiles) issued = stage_block(tc, bnext, tc % kStages);
+    bnext = tc + 1 < ntiles ? block_id((tc + 1) * (kKv / kBs) + bs) : -1;
+    bf16x8 pb[4];
+    qk(lds + ((j + 1) % kStages) * STAGE, mneg, sn);
+    probs(sc, pb);
+    pv(lds + (j % kStages) * STAGE, pb);
+    if (MASK) mask(sn, (j + 1) * kKv);
+    mx = rowmax(sn);
+    // masked steps may spill registers to scratch memory: wait for everything
+    step_barrier(issued && !MASK);
+  };
+  using F = std::false_type;
+  using T = std::true_type;
+  const int last = ntiles - 1;
+  int j = 0;
+  // steps whose successor needs no mask, then the rest; two per iteration so
+  // the S buffers alternate without copies
+  auto run = [&](auto maskc, int end) __attribute__((always_inline)) {
+    for (; j + 1 < end; j += 2) {
+      step(maskc, j, sa, sb);
+      step(maskc, j + 1, sb, sa);
+    }
+    if (j < end) {
+      step(maskc, j, sa, sb);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) sa[h] = sb[h];
+      ++j;
+    }
+  };
+  run(F{}, min(n_full - 1, last));
+  run(T{}, last);
+  {
+    rebase(sa);
+    bf16x8 pb[4];
+    probs(sa, pb);
+    pv(lds + (last % kStages) * STAGE, pb);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -380,13 +565,14 @@ extern "C" cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_
   cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &rows);
   if (st != CW_OK) return st;
   if (rows == 0) return cw::ok();
-  const int cph = head_dim / 8;
-  if (rows > INT32_MAX) return cw::fail(CW_EUNSUPPORTED, "kv_append: batch too large");
-  hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(rows)), dim3(kThreads), 0,
+  int64_t units = 0;   // blocks of suffix rows
+  for (int32_t r = 0; r < batch; ++r) units += (cu_suffix_host[r + 1] - cu_suffix_host[r] + kBs - 1) / kBs;
+  if (units > INT32_MAX) return cw::fail(CW_EUNSUPPORTED, "kv_append: batch too large");
+  hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(units)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(k_new),
                      static_cast<const u32x4*>(v_new), static_cast<u32x4*>(k_cache),
-                     static_cast<u32x4*>(v_cache), block_table, bt_stride, cu_suffix_dev,
-                     prefix_len_dev, batch, num_kv_heads, cph, num_blocks);
+                     static_cast<uint16_t*>(v_cache), block_table, bt_stride, cu_suffix_dev,
+                     prefix_len_dev, batch, num_kv_heads, head_dim, num_blocks);
   return check_launch("kv_append launch");
 }
 
@@ -429,11 +615,11 @@ extern "C" cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, 
   auto* pp = reinterpret_cast<const int4*>(plan_dev);
   auto* op = static_cast<uint16_t*>(out);
   if (head_dim == 128)
-    hipLaunchKernelGGL(suffix_prefill_attn_kernel<128>, dim3(unsigned(num_tiles)), dim3(kThreads), 0, s,
+    hipLaunchKernelGGL(suffix_prefill_attn_kernel<128>, dim3(unsigned(num_tiles)), dim3(kAttnThreads), 0, s,
                        qp, kp, vp, block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch,
                        num_q_heads, num_kv_heads, group, per_tile, num_blocks, c_log2, op);
   else
-    hipLaunchKernelGGL(suffix_prefill_attn_kernel<64>, dim3(unsigned(num_tiles)), dim3(kThreads), 0, s,
+    hipLaunchKernelGGL(suffix_prefill_attn_kernel<64>, dim3(unsigned(num_tiles)), dim3(kAttnThreads), 0, s,
                        qp, kp, vp, block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch,
                        num_q_heads, num_kv_heads, group, per_tile, num_blocks, c_log2, op);
   return check_launch("suffix_prefill_attn launch");

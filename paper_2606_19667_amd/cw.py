@@ -25,6 +25,7 @@ CW_EUNSUPPORTED = -2
 CW_ENOSPC = -3
 CW_EHIP = -4
 BLOCK_SIZE = 16
+TILE_ROWS = 256    # packed query rows (heads x positions) of one attention tile (cw.h)
 
 _i32 = ctypes.c_int32
 _i64 = ctypes.c_int64
@@ -287,6 +288,12 @@ class BatchMeta:
         return _ptr(a, ctypes.c_int32)
 
 
+def _cache_shapes_ok(k_cache: torch.Tensor, v_cache: torch.Tensor, hkv: int, D: int) -> bool:
+    """K blocks are [slot][d], V blocks [d][slot]; both caches hold the same blocks."""
+    return (k_cache.dim() == 4 and v_cache.dim() == 4 and tuple(k_cache.shape[1:]) == (hkv, BLOCK_SIZE, D)
+            and tuple(v_cache.shape) == (k_cache.shape[0], hkv, D, BLOCK_SIZE))
+
+
 def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor,
               v_cache: torch.Tensor, stream=None) -> None:
     """cw_kv_append: write the suffix K/V rows into their cache blocks."""
@@ -294,8 +301,8 @@ def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache
     for name, t in (("k_new", k_new), ("v_new", v_new)):
         if tuple(t.shape) != (meta.total_rows, hkv, D):
             raise ValueError(f"{name} must be [{meta.total_rows}, {hkv}, {D}], got {tuple(t.shape)}")
-    if k_cache.dim() != 4 or tuple(k_cache.shape[1:]) != (hkv, BLOCK_SIZE, D) or v_cache.shape != k_cache.shape:
-        raise ValueError("caches must be [num_blocks, Hkv, 16, D]")
+    if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
     _check(_lib.cw_kv_append(_dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
                              _dev(k_cache, torch.bfloat16, "k_cache"), _dev(v_cache, torch.bfloat16, "v_cache"),
                              _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
@@ -310,8 +317,8 @@ def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
     hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
     if tuple(q.shape) != (meta.total_rows, hq, D):
         raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
-    if k_cache.dim() != 4 or tuple(k_cache.shape[1:]) != (hkv, BLOCK_SIZE, D) or v_cache.shape != k_cache.shape:
-        raise ValueError("caches must be [num_blocks, Hkv, 16, D]")
+    if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
     if out is None:
         out = torch.empty_like(q)
     elif tuple(out.shape) != tuple(q.shape):
@@ -429,8 +436,8 @@ class BatchRunner:
                             ("v_new", v_new, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
                             ("v_cache", v_cache, torch.bfloat16), ("out", out, torch.bfloat16)):
             _dev(t, dt, name)
-        if k_cache.dim() != 4 or tuple(k_cache.shape[1:]) != (hkv, BLOCK_SIZE, D) or v_cache.shape != k_cache.shape:
-            raise ValueError("caches must be [num_blocks, Hkv, 16, D]")
+        if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+            raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
         self._tensors = (q, k_new, v_new, k_cache, v_cache, out)
         s = _stream(stream)
         p = self._p

@@ -88,25 +88,49 @@ def _cleanup():
 
 
 # ------------------------------------------------------------------ append
-@pytest.mark.parametrize("make", [W.tiny_single, W.llama8b_single,
-                                  lambda: W.llama8b_trace_batch(seed=1, batch=6, warmup=12)])
-def test_kv_append_cache_image_is_bit_exact(make):
-    w = make()
-    _say(f"kv_append {w.name}")
+def _append_check(w):
     db = B.materialize(w, keep_host=[])
     kb, vb = _bits(db.k_cache), _bits(db.v_cache)
     expect_k = OP.kv_append_image(kb, _bits(db.k_new), db.sched.block_table, db.sched.cu_suffix,
                                   db.sched.prefix_len, w.block_size)
     expect_v = OP.kv_append_image(vb, _bits(db.v_new), db.sched.block_table, db.sched.cu_suffix,
-                                  db.sched.prefix_len, w.block_size)
+                                  db.sched.prefix_len, w.block_size, layout="d_slot")
     cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
     torch.cuda.synchronize()
     assert np.array_equal(_bits(db.k_cache), expect_k)
     assert np.array_equal(_bits(db.v_cache), expect_v)
+    return db
+
+
+@pytest.mark.parametrize("make", [W.tiny_single, W.llama8b_single,
+                                  lambda: W.llama8b_trace_batch(seed=1, batch=6, warmup=12)])
+def test_kv_append_cache_image_is_bit_exact(make):
+    w = make()
+    _say(f"kv_append {w.name}")
+    db = _append_check(w)
     if w.name.startswith("tiny"):
         used = set(db.sched.block_table[0, :6].tolist())
         for b in set(range(8)) - used:           # two unreferenced blocks keep their sentinel
             assert (_bits(db.k_cache)[b] == B.SENTINEL_BITS).all()
+            assert (_bits(db.v_cache)[b] == B.SENTINEL_BITS).all()
+    _cleanup()
+
+
+@pytest.mark.parametrize("hq,hkv,D,nreq", [(8, 2, 128, 8), (16, 1, 64, 8), (48, 24, 128, 8),
+                                           (40, 20, 64, 8), (8, 8, 128, 70)])
+def test_kv_append_ragged_bit_exact(hq, hkv, D, nreq):
+    """Partial and empty blocks, head counts that take several staging passes,
+    and more requests than one wave scans at a time."""
+    if nreq == 8:
+        S = [1, 15, 16, 17, 600, 0, 33, 129]
+        P = [0, 16, 48, 0, 1024, 32, 1008, 64]
+    else:
+        rng = np.random.default_rng(nreq)
+        S = [int(x) if x % 7 else 0 for x in rng.integers(0, 40, size=nreq)]
+        P = [16 * int(x) for x in rng.integers(0, 4, size=nreq)]
+    w = _ragged(hq, hkv, D, S, P, seed=hq + D + nreq)
+    _say(f"kv_append {w.name} nreq={nreq}")
+    _append_check(w)
     _cleanup()
 
 

@@ -23,7 +23,7 @@ def test_exports_every_declared_symbol():
     lib = ctypes.CDLL(cw.LIB_PATH)
     for name in declared:
         assert hasattr(lib, name), name
-    assert cw.abi_version() == 1
+    assert cw.abi_version() == 2
 
 
 @pytest.mark.parametrize("n", [0, 1, 15, 16, 17, 100, 1408])
@@ -199,7 +199,7 @@ def test_plan_covers_every_row_once(shape):
         P = rng.integers(0, 60, size=B) * 16
         cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
         plan, n = cw.suffix_prefill_plan(cu, P, hq, hkv, 128)
-        per = 128 // (hq // hkv)
+        per = cw.TILE_ROWS // (hq // hkv)
         seen = _plan_rows(plan, n, cu, hkv, per)
         assert len(seen) == int(S.sum()) * hkv and set(seen.values()) == {1}
         real = [plan[4 * i:4 * i + 4] for i in range(n) if plan[4 * i] >= 0]
@@ -249,7 +249,7 @@ def test_plan_writes_exactly_plan_words(grouped):
     assert st == cw.CW_OK and 4 * n.value == words
     assert (buf[words:] == -7).all()
     assert _grouped(buf[:words], n.value, 8) == grouped
-    seen = _plan_rows(buf, n.value, cu, 8, 32)
+    seen = _plan_rows(buf, n.value, cu, 8, cw.TILE_ROWS // 4)
     assert len(seen) == int(S.sum()) * 8 and set(seen.values()) == {1}
 
 
@@ -277,7 +277,7 @@ def _attn(cu, plen, hq=32, hkv=8, d=128, bs=16, stride=100, scale=0.1, ntiles=No
     cu_a, cu_p = _arr(cu)
     pl_a, pl_p = _arr(plen)
     if ntiles is None:
-        per = max(1, 128 // max(1, hq // hkv))
+        per = max(1, cw.TILE_ROWS // max(1, hq // hkv))
         ntiles = sum(math.ceil((cu[i + 1] - cu[i]) / per) for i in range(len(plen))) * hkv
     d_ = _dummy()
     return cw.lib().cw_suffix_prefill_attn(d_, d_, d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d,

@@ -310,15 +310,44 @@ def test_append_image_hand_example():
     assert out[3].sum() == 0 and out[2].sum() == 0
 
 
-def test_append_image_vectorized_matches_loops():
+def test_append_image_transposed_hand_example():
+    cache = np.zeros((4, 1, 2, 4), dtype=np.uint16)      # [NB, Hkv, D, bs]
+    new = np.arange(1, 1 + 5 * 1 * 2, dtype=np.uint16).reshape(5, 1, 2)
+    bt = np.array([[3, 1, 0]], dtype=np.int32)
+    out = paged.kv_append_image(cache, new, bt, [0, 5], [4], block_size=4, layout="d_slot")
+    # tokens 4..7 -> block 1 slots 0..3: d = 0 row holds 1, 3, 5, 7; d = 1 row 2, 4, 6, 8
+    assert out[1, 0].tolist() == [[1, 3, 5, 7], [2, 4, 6, 8]]
+    assert out[0, 0, :, 0].tolist() == [9, 10] and out[0, 0, :, 1:].sum() == 0
+    assert out[3].sum() == 0 and out[2].sum() == 0
+    with pytest.raises(ValueError):
+        paged.kv_append_image(cache, new, bt, [0, 5], [4], block_size=4, layout="dslot")
+
+
+@pytest.mark.parametrize("layout", ["slot_d", "d_slot"])
+def test_append_image_vectorized_matches_loops(layout):
     rng = np.random.default_rng(8)
-    cache = rng.integers(0, 65535, size=(12, 2, 4, 3), dtype=np.uint16)
+    shape = (12, 2, 4, 3) if layout == "slot_d" else (12, 2, 3, 4)
+    cache = rng.integers(0, 65535, size=shape, dtype=np.uint16)
     P = [4, 0, 8]
     S = [5, 3, 1]
     cu = np.concatenate([[0], np.cumsum(S)])
     new = rng.integers(0, 65535, size=(cu[-1], 2, 3), dtype=np.uint16)
     bt = np.array([[0, 5, 7, 11], [2, 3, 1, 1], [9, 10, 4, 4]], dtype=np.int32)
-    a = paged.kv_append_image(cache, new, bt, cu, P, 4)
-    b = paged.kv_append_image_loops(cache, new, bt, cu, P, 4)
+    a = paged.kv_append_image(cache, new, bt, cu, P, 4, layout=layout)
+    b = paged.kv_append_image_loops(cache, new, bt, cu, P, 4, layout=layout)
     assert np.array_equal(a, b)
     assert np.array_equal(a[6], cache[6]) and np.array_equal(a[8], cache[8])
+
+
+def test_append_image_layouts_are_transposes():
+    """The per-block transposed image is the transpose of the row-major one."""
+    rng = np.random.default_rng(9)
+    cache = rng.integers(0, 65535, size=(10, 3, 4, 5), dtype=np.uint16)
+    S = [7, 2, 9]
+    P = [0, 8, 4]
+    cu = np.concatenate([[0], np.cumsum(S)])
+    new = rng.integers(0, 65535, size=(cu[-1], 3, 5), dtype=np.uint16)
+    bt = np.array([[0, 1, 2, 9], [3, 4, 5, 9], [6, 7, 8, 9]], dtype=np.int32)
+    a = paged.kv_append_image(cache, new, bt, cu, P, 4)
+    b = paged.kv_append_image(cache.swapaxes(2, 3), new, bt, cu, P, 4, layout="d_slot")
+    assert np.array_equal(a.swapaxes(2, 3), b)
