@@ -94,7 +94,83 @@ def make_workload(name: str, seed: int):
         return W.long_context(name.rsplit("-", 1)[1], seed)
     if name == "tiny":
         return W.tiny_single(seed)
+    if name == "llama8b-question-only":
+        return W.question_only(seed)
     raise SystemExit(f"unknown workload {name}")
+
+
+def percentiles_us(times_ms):
+    t = np.asarray(times_ms, dtype=np.float64) * 1e3
+    return {"median": round(float(np.median(t)), 2), "p10": round(float(np.percentile(t, 10)), 2),
+            "p90": round(float(np.percentile(t, 90)), 2), "n": int(t.size)}
+
+
+def timed_calls(fn, stream, n: int, between=None):
+    """Per-call durations (ms) of `fn` with HIP events on `stream`; `between`
+    runs before each call, outside the timed interval."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in evs:
+        if between is not None:
+            between()
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
+
+
+def host_timing(w, snapshot, stride: int, reps: int = 20):
+    """Host side per request, in microseconds: cw_schedule_batch over the batch
+    (chained hashes, prefix match, allocation, commit) and the greedy
+    knowledge-tree ordering of the trace's queries (Python)."""
+    from paper_2606_19667_amd import cw
+    from paper_2606_19667_amd import workload as W
+    toks = [p.tokens(w.seed) for p in w.prompts]
+    best = float("inf")
+    for _ in range(reps):
+        pool = snapshot.clone()
+        t0 = time.perf_counter()
+        cw.schedule_batch(pool, toks, stride, w.block_size)
+        best = min(best, time.perf_counter() - t0)
+        pool.close()
+    res = {"schedule_us_per_request": round(best * 1e6 / w.batch, 2)}
+    if w.warmup:
+        qs = W.synthetic_trace(len(w.warmup) + w.batch, seed=w.seed)
+        tree = W.KnowledgeTree()
+        t0 = time.perf_counter()
+        for docs in qs:
+            order, _, _ = tree.order(docs)
+            tree.insert(order)
+        res["ordering_us_per_request"] = round((time.perf_counter() - t0) * 1e6 / len(qs), 2)
+        res["ordering_impl"] = "Python greedy knowledge-tree walk + insert"
+    return res
+
+
+def question_only_point(seed: int, stream):
+    """Diagnostic short-suffix point: 16 8B-shaped requests with the whole
+    1344-token evidence prefix cached and a 64-token question to prefill.
+    Arithmetic intensity is below the ridge, so it is judged by GB/s."""
+    import torch
+    from paper_2606_19667_amd import batch as B
+    from paper_2606_19667_amd import cw
+    w = make_workload("llama8b-question-only", seed)
+    db = B.materialize(w, device="cuda", keep_host=[])
+    cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
+    out = torch.empty_like(db.q)
+    fn = lambda: cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale, out=out, stream=stream)
+    for _ in range(10):
+        fn()
+    t = percentiles_us(timed_calls(fn, stream, 50))
+    S = np.diff(db.sched.cu_suffix)
+    P = db.sched.prefix_len
+    hq, hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
+    fl = attention_flops(P, S, hq, D)
+    by = attention_bytes(P, S, hq, hkv, D)
+    sec = t["median"] * 1e-6
+    return {"workload": w.name, "attention_us": t, "GFLOP": round(fl / 1e9, 3), "algorithmic_MB": round(by / 1e6, 2),
+            "achieved_GBps": round(by / sec / 1e9, 1), "frac_hbm": round(by / sec / 1e9 / PEAK_HBM_GBS, 4),
+            "achieved_TFLOPs": round(fl / sec / 1e12, 2), "bound": "hbm"}
 
 
 def cpu_baseline(w, sched, budget_s: float = 12.0):
@@ -255,6 +331,14 @@ def main() -> int:
     rn = runners[(args.warmup + args.steps - 1) % 2] if args.steps else runners[0]
     attn_ms = kernel_ms(rn.attention, max(args.steps, 10))
     app_ms = kernel_ms(rn.kv_append, max(args.steps, 10))
+    print("[bench] per-call, cold-cache and host timings", file=sys.stderr, flush=True)
+    # Per-call durations (hot caches) and with a 512 MB scratch buffer written
+    # between calls, which evicts the K/V from L2 and the 256 MB MALL.
+    hot = percentiles_us(timed_calls(rn.attention, stream, 50))
+    scratch = torch.empty(256 << 20, dtype=torch.bfloat16, device=dev)
+    cold = percentiles_us(timed_calls(rn.attention, stream, 20, between=lambda: scratch.fill_(1.0)))
+    del scratch
+    host = host_timing(w, snapshot, stride) if trace_mode else None
 
     achieved = flops / (attn_ms * 1e-3) / 1e12
     res = {
@@ -285,9 +369,17 @@ def main() -> int:
                      "traffic": counted_traffic(args.workload),
                      "kernel": "suffix_prefill_attn_kernel<128>",
                      "algorithmic_bytes": int(attention_bytes(P, S, hq, hkv, D))},
+        "attention_call_us": hot,
+        "attention_cold_us": cold,
     }
+    if host is not None:
+        res["host"] = host
     del db, runners, out
     torch.cuda.empty_cache()
+    if args.workload == "llama8b-trace-b16":
+        print("[bench] question-only diagnostic point", file=sys.stderr, flush=True)
+        res["diagnostic_question_only"] = question_only_point(args.seed, stream)
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, sched)

@@ -279,6 +279,16 @@ def llama8b_single(seed: int = 0) -> Workload:
                     prefix_lens=[832])
 
 
+def question_only(seed: int = 0, batch: int = 16) -> Workload:
+    """`batch` Llama-3-8B-shaped requests whose whole evidence prefix is cached
+    (instruction + 5 chunks of 256 = 1344 tokens): only the 64-token question is
+    prefilled. The deepest reuse the ordering aims for; a short-suffix shape."""
+    prompts = [rag_prompt(r, range(5 * r, 5 * r + 5), 256) for r in range(batch)]
+    P = INSTR_TOKENS + 5 * 256
+    return Workload(f"llama8b-question-only-b{batch}-p{P}-s{QUESTION_TOKENS}", 32, 8, 128, 16, prompts,
+                    seed=seed, prefix_lens=[P] * batch, free_order_key=(64,))
+
+
 def serve_trace(queries, tree: KnowledgeTree, chunk_tokens: int, uid0: int = 0):
     """Order each query with the tree, insert it after serving; returns prompts
     and the greedy depth (documents) of each."""

@@ -169,6 +169,15 @@ def test_attention_trace_batch16_sampled():
     _cleanup()
 
 
+def test_attention_question_only_full():
+    """The short-suffix shape: whole evidence prefix cached, 64-token questions."""
+    w = W.question_only()
+    _say(f"attention {w.name}")
+    db = B.materialize(w)
+    _compare_full(db, _run(db))
+    _cleanup()
+
+
 def _ragged(hq, hkv, D, S, P, seed):
     prompts = [W.Prompt(uid=i, segments=[(W.SEG_QUESTION_BASE + i, p + s)]) for i, (s, p) in enumerate(zip(S, P))]
     return W.Workload(f"ragged-{hq}q{hkv}kv-d{D}", hq, hkv, D, 16, prompts, seed=seed, prefix_lens=list(P),

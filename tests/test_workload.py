@@ -139,3 +139,14 @@ def test_named_shapes():
     w = W.long_context("high")
     assert w.prompts[0].length == 10368
     assert all(64 + 512 * 12 <= p <= 64 + 512 * 16 for p in w.prefix_lens)
+
+
+def test_question_only_shape():
+    w = W.question_only()
+    assert w.batch == 16 and all(p.length == 1408 for p in w.prompts)
+    assert w.prefix_lens == [1344] * 16
+    # the 4 instruction blocks are common; every later block is the request's own
+    keys = [p.block_keys(16) for p in w.prompts]
+    assert all(k[:4] == keys[0][:4] for k in keys)
+    later = [set(k[4:]) for k in keys]
+    assert all(not (later[a] & later[b]) for a in range(16) for b in range(a + 1, 16))
