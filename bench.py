@@ -168,9 +168,25 @@ def question_only_point(seed: int, stream):
     fl = attention_flops(P, S, hq, D)
     by = attention_bytes(P, S, hq, hkv, D)
     sec = t["median"] * 1e-6
-    return {"workload": w.name, "attention_us": t, "GFLOP": round(fl / 1e9, 3), "algorithmic_MB": round(by / 1e6, 2),
-            "achieved_GBps": round(by / sec / 1e9, 1), "frac_hbm": round(by / sec / 1e9 / PEAK_HBM_GBS, 4),
-            "achieved_TFLOPs": round(fl / sec / 1e12, 2), "bound": "hbm"}
+    res = {"workload": w.name, "attention_us": t, "GFLOP": round(fl / 1e9, 3), "algorithmic_MB": round(by / 1e6, 2),
+           "achieved_GBps": round(by / sec / 1e9, 1), "frac_hbm": round(by / sec / 1e9 / PEAK_HBM_GBS, 4),
+           "achieved_TFLOPs": round(fl / sec / 1e12, 2), "bound": "hbm"}
+    # the split-KV path (cw_suffix_prefill_attn_split, merge included)
+    res["split"] = {}
+    for n in sorted({cw.split_count(db.meta), 2, 4}):
+        ws = torch.empty(cw.split_workspace_bytes(db.meta, n), dtype=torch.uint8, device="cuda")
+        fs = lambda: cw.suffix_prefill_attn_split(db.meta, db.q, db.k_cache, db.v_cache, db.scale, num_splits=n,
+                                                  workspace=ws, out=out, stream=stream)
+        for _ in range(10):
+            fs()
+        ts = percentiles_us(timed_calls(fs, stream, 50))
+        sec = ts["median"] * 1e-6
+        res["split"][str(n)] = {"attention_us": ts, "achieved_GBps": round(by / sec / 1e9, 1),
+                                "frac_hbm": round(by / sec / 1e9 / PEAK_HBM_GBS, 4),
+                                "workspace_MB": round(ws.numel() / 1e6, 2)}
+        del ws
+    res["split_auto"] = cw.split_count(db.meta)
+    return res
 
 
 def cpu_baseline(w, sched, budget_s: float = 12.0):

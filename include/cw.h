@@ -237,6 +237,52 @@ cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void*
                                  float softmax_scale, const int32_t* plan_dev, int32_t num_tiles,
                                  void* out, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Device: split-KV variant of cw_suffix_prefill_attn, for batches with few
+ * tiles (short suffixes such as a question after a fully cached evidence
+ * prefix: paper Sec. 1 and 3.3, the reuse the ordering aims for). Same result
+ * up to rounding, same arguments and plan.
+ *
+ * Each plan tile's key range is divided into num_splits runs of whole 64-key
+ * steps, processed by separate workgroups; each run's attention over its own
+ * keys (normalised O in fp32 and its base-2 log-sum-exp per row) is written to
+ * `workspace`, then combined exactly as by cw_lse_merge into out (bf16).
+ *   num_splits       1 .. 64
+ *   workspace        caller-owned device memory of at least
+ *                    cw_suffix_prefill_split_workspace_bytes(total_s, Hq, D,
+ *                    num_splits) bytes; overwritten by the call
+ * Errors as cw_suffix_prefill_attn, plus CW_EINVAL for num_splits out of range
+ * or a missing / too small workspace.
+ * cw_suffix_prefill_split_workspace_bytes returns the size, or a negative
+ * cw_status for invalid arguments. */
+int64_t cw_suffix_prefill_split_workspace_bytes(int64_t total_rows, int32_t num_q_heads, int32_t head_dim,
+                                                int32_t num_splits);
+cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* block_table, int32_t bt_stride,
+                                       const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
+                                       const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                       int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                                       float softmax_scale, const int32_t* plan_dev, int32_t num_tiles,
+                                       int32_t num_splits, void* workspace, int64_t workspace_bytes,
+                                       void* out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Device: merge of attention results computed over disjoint key sets (the
+ * pieces of cw_suffix_prefill_attn_split; also how partial results over a
+ * prefix split across GPUs would be combined). Softmax over a union of key
+ * sets, written out by log-sum-exp:
+ *   M = max_p lse[p][i],  w_p = 2^(lse[p][i] - M)
+ *   out[i][:] = sum_p w_p * o[p][i][:] / sum_p w_p        (bf16, RNE)
+ *   partial_o    device fp32 [num_parts, rows, head_dim], each part normalised
+ *   partial_lse  device fp32 [num_parts, rows]: log2 of the part's sum of
+ *                exp(scaled score); -inf for a part with no keys (skipped).
+ *                A row whose parts are all -inf is written as zeros.
+ * CW_EINVAL: NULL pointer, num_parts < 1, rows < 0.
+ * CW_EUNSUPPORTED: head_dim not a multiple of 8 in [8, 1024]. */
+cw_status cw_lse_merge(const void* partial_o, const void* partial_lse, int32_t num_parts, int64_t rows,
+                       int32_t head_dim, void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -150,3 +150,62 @@ def attention_flops(prefix_lens, suffix_lens, num_q_heads: int, head_dim: int) -
     for p, s in zip(prefix_lens, suffix_lens):
         pairs += s * p + s * (s + 1) // 2
     return 4 * head_dim * num_q_heads * pairs
+
+
+# ---------------------------------------------------------------------------
+# Attention over a subset of the keys, and the log-sum-exp merge of such parts.
+#
+# Softmax over a union of disjoint key sets factors through per-set sums: with
+# Z_A = sum_{j in A} exp(s_j), softmax over A u B weights the set-A output
+# O_A = sum_{j in A} exp(s_j) v_j / Z_A by Z_A / (Z_A + Z_B). The parts are
+# therefore kept as (O_A, log Z_A); the merge is the definition of the softmax
+# written through those sums. The library reports log Z in base 2
+# (log2 Z = ln Z / ln 2), and so do these functions.
+# ---------------------------------------------------------------------------
+def suffix_prefill_partial(q, k, v, prefix_len: int, scale: float, key_lo: int, key_hi: int):
+    """Attention of the suffix rows over the keys j in [key_lo, key_hi) that
+    each row may see (j <= prefix_len + i).
+
+    Returns (o [S, Hq, D], lse2 [S, Hq]) in float64: o is normalised over the
+    part's visible keys and lse2 = log2(sum_j exp(s_j)) over them; a row that
+    sees none of the part's keys gets o = 0 and lse2 = -inf.
+    """
+    q = _as_f64(q)
+    k = _as_f64(k)
+    v = _as_f64(v)
+    _check_shapes(q, k, v, prefix_len)
+    S, Hq, D = q.shape
+    L, Hkv, _ = k.shape
+    G = Hq // Hkv
+    o = np.zeros((S, Hq, D), dtype=np.float64)
+    lse2 = np.full((S, Hq), -np.inf, dtype=np.float64)
+    j = np.arange(L)
+    for i in range(S):
+        keys = j[(j >= key_lo) & (j < key_hi) & (j <= prefix_len + i)]
+        if keys.size == 0:
+            continue
+        for h in range(Hq):
+            g = h // G
+            s = scale * (k[keys, g, :] @ q[i, h, :])
+            m = s.max()
+            w = np.exp(s - m)
+            o[i, h] = (w @ v[keys, g, :]) / w.sum()
+            lse2[i, h] = (m + math.log(w.sum())) / math.log(2.0)
+    return o, lse2
+
+
+def lse_merge(parts_o, parts_lse2) -> np.ndarray:
+    """Combine parts computed over disjoint key sets.
+
+    parts_o [n, rows, D], parts_lse2 [n, rows] (base 2, -inf for an empty
+    part) -> [rows, D]: sum_p 2^(lse_p) o_p / sum_p 2^(lse_p), evaluated
+    relative to the largest lse_p; a row with every part empty is zero.
+    """
+    o = _as_f64(parts_o)
+    lse = _as_f64(parts_lse2)
+    m = lse.max(axis=0)                                              # [rows]
+    finite = np.isfinite(m)
+    w = np.where(np.isfinite(lse), np.exp2(lse - np.where(finite, m, 0.0)[None, :]), 0.0)   # [n, rows]
+    tot = w.sum(axis=0)
+    out = np.einsum("pr,prd->rd", w, o)
+    return np.where(tot[:, None] > 0, out / np.where(tot > 0, tot, 1.0)[:, None], 0.0)

@@ -44,6 +44,7 @@ constexpr int kBs = cw::kBlockSize;
 constexpr int kKv = cw::kKvTile;
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Two floats to two bfloat16 (round to nearest even) in one dword, low first.
@@ -240,20 +241,29 @@ __device__ __forceinline__ bf16x8 scale_bf16x8(u32x4 raw, float c) {
   return __builtin_bit_cast(bf16x8, u32x4{o[0], o[1], o[2], o[3]});
 }
 
-template <int D>
+// SPLIT: the key range of each tile is divided into num_splits runs of whole
+// steps processed by separate workgroups (workgroup s * num_tiles + i takes run s
+// of plan entry i); each writes, for its rows, the attention over its keys only:
+// O normalised in fp32 to part_o[s][row][d] and the base-2 log-sum-exp of the
+// scaled scores to part_lse[s][row] (row = suffix row * Hq + head), -inf when
+// no key of the run is visible. lse_merge_kernel combines the runs.
+template <int D, bool SPLIT>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
                                 const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
                                 int bt_stride, const int32_t* __restrict__ cu,
                                 const int32_t* __restrict__ plen, const int4* __restrict__ plan,
                                 int batch, int hq, int hkv, int group, int per_tile, int num_blocks,
-                                float c_log2, uint16_t* __restrict__ out) {
+                                float c_log2, uint16_t* __restrict__ out, int num_splits, int num_tiles,
+                                int64_t part_rows, float* __restrict__ part_o, float* __restrict__ part_lse) {
   using G = AttnGeom<D>;
   constexpr int KS = G::KS, DT = G::DT, RB = G::RB, NC = G::NC, LPW = G::LPW, RPL = G::RPL;
   constexpr int KTILE = G::KTILE, BLK = G::BLK, STAGE = G::STAGE;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE];
 
-  const int4 item = plan[blockIdx.x];
+  const int tile = SPLIT ? int(blockIdx.x % unsigned(num_tiles)) : int(blockIdx.x);
+  const int split = SPLIT ? int(blockIdx.x / unsigned(num_tiles)) : 0;
+  const int4 item = plan[tile];
   const int r = item.x, g = item.y, row0 = item.z;
   if (r < 0 || r >= batch || g < 0 || g >= hkv) return;
   const int cu0 = cu[r];
@@ -264,8 +274,15 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   const int nvalid = min(per_tile, S - row0);
   const int kv_end = P + row0 + nvalid;
   const int ntiles = (kv_end + kKv - 1) / kKv;
-  // steps 0 .. n_full - 1 are visible to every row of the tile (no mask)
-  const int n_full = min(ntiles, (P + row0 + 1) / kKv);
+  // this workgroup's steps: tbeg .. tbeg + nsteps - 1 of the tile's key range
+  int tbeg = 0, nsteps = ntiles;
+  if (SPLIT) {
+    const int per = (ntiles + num_splits - 1) / num_splits;
+    tbeg = split * per;
+    nsteps = max(0, min(ntiles, tbeg + per) - tbeg);
+  }
+  // local steps 0 .. n_full - 1 are visible to every row of the tile (no mask)
+  const int n_full = max(0, min(nsteps, (P + row0 + 1) / kKv - tbeg));
   const int nblk = (L + kBs - 1) / kBs;
   const int32_t* btr = bt + int64_t(r) * bt_stride;
 
@@ -283,6 +300,20 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   const int qpos = P + row0 + pos;  // keys 0 .. qpos are visible
   const int64_t qrow = int64_t(cu0) + row0 + pos;
   const int head = g * group + hh;
+
+  if (SPLIT && nsteps == 0) {   // no key of this run: an empty part
+    if (row_ok) {
+      const int64_t prow = int64_t(split) * part_rows + qrow * hq + head;
+      float* po = part_o + prow * D;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq)
+          *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (half == 0) part_lse[prow] = -INFINITY;
+    }
+    return;
+  }
 
   bf16x8 qf[KS];
   if (row_ok) {
@@ -322,7 +353,7 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   // Stages step t's block of this wave into stage st; returns whether it used
   // the load-to-LDS path (whose completion the caller then waits for).
   auto stage_block = [&](int t, int b, int st) __attribute__((always_inline)) -> bool {
-    const int key0 = t * kKv + bs * kBs;
+    const int key0 = (tbeg + t) * kKv + bs * kBs;
     const uint8_t* src = reinterpret_cast<const uint8_t*>(cache) +
                          (int64_t(b < 0 ? 0 : b) * hkv + g) * (kBs * RB);
     uint8_t* dst = lds + st * STAGE + dst0;
@@ -386,7 +417,7 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   };
   // Causal mask of the step starting at key k0.
   auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
-    const int lim = qpos - k0;
+    const int lim = qpos - k0;   // k0: absolute first key of the step
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -445,17 +476,23 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   // ---- prologue: stage steps 0 and 1 (and K of step 2); S(0) with the exact
   // row maximum as base
   {
-    const int n0 = min(ntiles, ahead);
-    for (int t = 0; t < n0; ++t) stage_block(t, block_id(t * (kKv / kBs) + bs), t);
+    const int n0 = min(nsteps, ahead);
+    for (int t = 0; t < n0; ++t) stage_block(t, block_id((tbeg + t) * (kKv / kBs) + bs), t);
   }
-  int bnext = ahead < ntiles ? block_id(ahead * (kKv / kBs) + bs) : -1;   // block copied in step 0
+  // block copied in step 0
+  int bnext = ahead < nsteps ? block_id((tbeg + ahead) * (kKv / kBs) + bs) : -1;
   step_barrier(false);
   f32x16 sa[2], sb[2];
   qk(lds, f32x16{}, sa);
-  if (n_full == 0) mask(sa, 0);
+  if (n_full == 0) mask(sa, tbeg * kKv);
   f32x16 mneg;   // -m in every element: the start of each S accumulator
   {
-    const float m0 = rowmax(sa);   // finite: key 0 is visible to every row
+    // Finite when the run's first step has a visible key for this row (always
+    // so for the first run: key 0 is visible to every row). A row that sees no
+    // key of the run's first step sees none of its later steps either (they
+    // hold higher keys), so any base serves it.
+    float m0 = rowmax(sa);
+    if (SPLIT && m0 == -INFINITY) m0 = 0.f;
 #pragma unroll
     for (int h = 0; h < 2; ++h) sa[h] -= m0;
 #pragma unroll
@@ -480,27 +517,27 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
       for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
     }
   };
-  // Step j < ntiles - 1: current S in sc, next S into sn. Stage of step t is
-  // t % 3; this wave copies step j + ahead into stage (j + ahead) % 3.
+  // Step j < nsteps - 1: current S in sc, next S into sn. Stage of local step
+  // t is t % 3; this wave copies step j + ahead into stage (j + ahead) % 3.
   auto step = [&](auto maskc, int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
     constexpr bool MASK = decltype(maskc)::value;
     rebase(sc);
     const int tc = j + ahead;
     bool issued = false;
-    if (tc < ntiles) issued = stage_block(tc, bnext, tc % kStages);
-    bnext = tc + 1 < ntiles ? block_id((tc + 1) * (kKv / kBs) + bs) : -1;
+    if (tc < nsteps) issued = stage_block(tc, bnext, tc % kStages);
+    bnext = tc + 1 < nsteps ? block_id((tbeg + tc + 1) * (kKv / kBs) + bs) : -1;
     bf16x8 pb[4];
     qk(lds + ((j + 1) % kStages) * STAGE, mneg, sn);
     probs(sc, pb);
     pv(lds + (j % kStages) * STAGE, pb);
-    if (MASK) mask(sn, (j + 1) * kKv);
+    if (MASK) mask(sn, (tbeg + j + 1) * kKv);
     mx = rowmax(sn);
     // masked steps may spill registers to scratch memory: wait for everything
     step_barrier(issued && !MASK);
   };
   using F = std::false_type;
   using T = std::true_type;
-  const int last = ntiles - 1;
+  const int last = nsteps - 1;
   int j = 0;
   // steps whose successor needs no mask, then the rest; two per iteration so
   // the S buffers alternate without copies
@@ -527,6 +564,22 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!row_ok) return;
+  if constexpr (SPLIT) {
+    const int64_t prow = int64_t(split) * part_rows + qrow * hq + head;
+    float* po = part_o + prow * D;
+    const bool any = l_tot > 0.f;
+    const float inv = any ? 1.f / l_tot : 0.f;
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq)
+        *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) =
+            f32x4{oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv, oacc[t][gq * 4 + 2] * inv,
+                  oacc[t][gq * 4 + 3] * inv};
+    // base-2 log-sum-exp of the scaled scores: the base plus log2 of the sum
+    if (half == 0) part_lse[prow] = any ? -mneg[0] + __log2f(l_tot) : -INFINITY;
+    return;
+  }
   const float inv = 1.f / l_tot;
   uint16_t* op = out + (qrow * hq + head) * D;
 #pragma unroll
@@ -538,6 +591,46 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
                     pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
       *reinterpret_cast<u32x2*>(op + d) = w;
     }
+}
+
+// ---------------------------------------------------------------------------
+// Log-sum-exp merge of attention results over disjoint key sets: for each row,
+// out = sum_p 2^(lse_p - M) o_p / sum_p 2^(lse_p - M), M = max_p lse_p, where o_p
+// is part p's normalised output and lse_p its base-2 log-sum-exp (-inf for a
+// part with no keys). One thread per row and 8 consecutive elements.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void lse_merge_kernel(const float* __restrict__ part_o,
+                                                             const float* __restrict__ part_lse,
+                                                             int num_parts, int64_t rows, int d,
+                                                             uint16_t* __restrict__ out) {
+  const int per_row = d / 8;
+  const int64_t u = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (u >= rows * per_row) return;
+  const int64_t row = u / per_row;
+  const int c = int(u - row * per_row);
+  float m = -INFINITY;
+  for (int p = 0; p < num_parts; ++p) m = fmaxf(m, part_lse[int64_t(p) * rows + row]);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  if (m != -INFINITY) {
+    for (int p = 0; p < num_parts; ++p) {
+      const float lp = part_lse[int64_t(p) * rows + row];
+      if (lp == -INFINITY) continue;
+      const float w = __builtin_amdgcn_exp2f(lp - m);
+      wsum += w;
+      const f32x4* src = reinterpret_cast<const f32x4*>(part_o + (int64_t(p) * rows + row) * d + c * 8);
+      const f32x4 a = src[0], b = src[1];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[e] = fmaf(w, a[e], acc[e]);
+        acc[4 + e] = fmaf(w, b[e], acc[4 + e]);
+      }
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const u32x4 o{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+                pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)};
+  *reinterpret_cast<u32x4*>(out + row * d + c * 8) = o;
 }
 
 cw_status check_launch(const char* what) {
@@ -576,6 +669,90 @@ extern "C" cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_
   return check_launch("kv_append launch");
 }
 
+namespace {
+
+// Checks shared by both attention entry points; fills the launch geometry.
+struct AttnShape {
+  int group = 0, per_tile = 0;
+  int64_t rows = 0;
+};
+cw_status check_attn(const char* what, const void* q, const void* k_cache, const void* v_cache,
+                     const int32_t* block_table, int32_t bt_stride, const int32_t* cu_suffix_dev,
+                     const int32_t* prefix_len_dev, const int32_t* cu_suffix_host,
+                     const int32_t* prefix_len_host, int32_t batch, int32_t num_q_heads,
+                     int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                     float softmax_scale, const int32_t* plan_dev, int32_t num_tiles, const void* out,
+                     AttnShape* shape) {
+  const std::string w(what);
+  if (!q || !k_cache || !v_cache || !block_table || !cu_suffix_dev || !prefix_len_dev || !out)
+    return cw::fail(CW_EINVAL, w + ": a required pointer is NULL");
+  if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0)
+    return cw::fail(CW_EINVAL, w + ": num_q_heads must be a positive multiple of num_kv_heads");
+  if (num_blocks < 1) return cw::fail(CW_EINVAL, w + ": num_blocks must be >= 1");
+  if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
+    return cw::fail(CW_EINVAL, w + ": softmax_scale must be finite and positive");
+  if (head_dim != 64 && head_dim != 128) return cw::fail(CW_EUNSUPPORTED, w + ": head_dim must be 64 or 128");
+  if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, w + ": block_size must be 16");
+  shape->group = num_q_heads / num_kv_heads;
+  if (shape->group > cw::kMaxGroup)
+    return cw::fail(CW_EUNSUPPORTED, w + ": more than 128 query heads per KV head");
+  cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &shape->rows);
+  if (st != CW_OK) return st;
+  shape->per_tile = cw::tile_positions(shape->group);
+  const int64_t need = cw::count_tiles(cu_suffix_host, batch, num_kv_heads, shape->per_tile);
+  if (num_tiles < need || int64_t(num_tiles) > need * cw::kNumXcd)
+    return cw::fail(CW_EINVAL, w + ": num_tiles " + std::to_string(num_tiles) + " does not match the batch (" +
+                                   std::to_string(need) + " tiles)");
+  if (num_tiles > 0 && !plan_dev) return cw::fail(CW_EINVAL, w + ": plan_dev is required");
+  return CW_OK;
+}
+
+template <bool SPLIT>
+void launch_attn(int head_dim, unsigned grid, hipStream_t s, const void* q, const void* k_cache,
+                 const void* v_cache, const int32_t* block_table, int32_t bt_stride,
+                 const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev, const int32_t* plan_dev,
+                 int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, const AttnShape& sh,
+                 int32_t num_blocks, float softmax_scale, void* out, int num_splits, int num_tiles,
+                 int64_t part_rows, float* part_o, float* part_lse) {
+  const float c_log2 = softmax_scale * 1.4426950408889634f;
+  auto* qp = static_cast<const uint16_t*>(q);
+  auto* kp = static_cast<const uint16_t*>(k_cache);
+  auto* vp = static_cast<const uint16_t*>(v_cache);
+  auto* pp = reinterpret_cast<const int4*>(plan_dev);
+  auto* op = static_cast<uint16_t*>(out);
+  if (head_dim == 128)
+    hipLaunchKernelGGL((suffix_prefill_attn_kernel<128, SPLIT>), dim3(grid), dim3(kAttnThreads), 0, s, qp, kp, vp,
+                       block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch, num_q_heads,
+                       num_kv_heads, sh.group, sh.per_tile, num_blocks, c_log2, op, num_splits, num_tiles,
+                       part_rows, part_o, part_lse);
+  else
+    hipLaunchKernelGGL((suffix_prefill_attn_kernel<64, SPLIT>), dim3(grid), dim3(kAttnThreads), 0, s, qp, kp, vp,
+                       block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch, num_q_heads,
+                       num_kv_heads, sh.group, sh.per_tile, num_blocks, c_log2, op, num_splits, num_tiles,
+                       part_rows, part_o, part_lse);
+}
+
+constexpr int kMaxSplits = 64;
+
+// Workspace of the split path: part_o [splits][rows][D] fp32, then part_lse
+// [splits][rows] fp32 at a 256-byte aligned offset.
+int64_t split_lse_offset(int64_t part_rows, int head_dim, int num_splits) {
+  return (int64_t(num_splits) * part_rows * head_dim * 4 + 255) / 256 * 256;
+}
+
+cw_status launch_merge(const float* part_o, const float* part_lse, int num_parts, int64_t rows, int head_dim,
+                       void* out, hipStream_t s) {
+  const int64_t units = rows * (head_dim / 8);
+  const int64_t grid = (units + kThreads - 1) / kThreads;
+  if (grid > INT32_MAX) return cw::fail(CW_EUNSUPPORTED, "lse_merge: too many rows");
+  if (grid == 0) return cw::ok();
+  hipLaunchKernelGGL(lse_merge_kernel, dim3(unsigned(grid)), dim3(kThreads), 0, s, part_o, part_lse, num_parts,
+                     rows, head_dim, static_cast<uint16_t*>(out));
+  return check_launch("lse_merge launch");
+}
+
+}  // namespace
+
 extern "C" cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void* v_cache,
                                             const int32_t* block_table, int32_t bt_stride,
                                             const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
@@ -584,43 +761,70 @@ extern "C" cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, 
                                             int32_t head_dim, int32_t block_size, int32_t num_blocks,
                                             float softmax_scale, const int32_t* plan_dev,
                                             int32_t num_tiles, void* out, void* stream) {
-  if (!q || !k_cache || !v_cache || !block_table || !cu_suffix_dev || !prefix_len_dev || !out)
-    return cw::fail(CW_EINVAL, "suffix_prefill_attn: a required pointer is NULL");
-  if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0)
-    return cw::fail(CW_EINVAL, "suffix_prefill_attn: num_q_heads must be a positive multiple of num_kv_heads");
-  if (num_blocks < 1) return cw::fail(CW_EINVAL, "suffix_prefill_attn: num_blocks must be >= 1");
-  if (!(softmax_scale > 0.f) || !std::isfinite(softmax_scale))
-    return cw::fail(CW_EINVAL, "suffix_prefill_attn: softmax_scale must be finite and positive");
-  if (head_dim != 64 && head_dim != 128)
-    return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn: head_dim must be 64 or 128");
-  if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn: block_size must be 16");
-  const int group = num_q_heads / num_kv_heads;
-  if (group > cw::kMaxGroup)
-    return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn: more than 128 query heads per KV head");
-  int64_t rows = 0;
-  cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &rows);
+  AttnShape sh;
+  cw_status st = check_attn("suffix_prefill_attn", q, k_cache, v_cache, block_table, bt_stride, cu_suffix_dev,
+                            prefix_len_dev, cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
+                            head_dim, block_size, num_blocks, softmax_scale, plan_dev, num_tiles, out, &sh);
   if (st != CW_OK) return st;
-  const int per_tile = cw::tile_positions(group);
-  const int64_t need = cw::count_tiles(cu_suffix_host, batch, num_kv_heads, per_tile);
-  if (num_tiles < need || int64_t(num_tiles) > need * cw::kNumXcd)
-    return cw::fail(CW_EINVAL, "suffix_prefill_attn: num_tiles " + std::to_string(num_tiles) +
-                                   " does not match the batch (" + std::to_string(need) + " tiles)");
-  if (num_tiles > 0 && !plan_dev) return cw::fail(CW_EINVAL, "suffix_prefill_attn: plan_dev is required");
-  if (rows == 0 || num_tiles == 0) return cw::ok();
-  const float c_log2 = softmax_scale * 1.4426950408889634f;
-  auto* s = static_cast<hipStream_t>(stream);
-  auto* qp = static_cast<const uint16_t*>(q);
-  auto* kp = static_cast<const uint16_t*>(k_cache);
-  auto* vp = static_cast<const uint16_t*>(v_cache);
-  auto* pp = reinterpret_cast<const int4*>(plan_dev);
-  auto* op = static_cast<uint16_t*>(out);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(suffix_prefill_attn_kernel<128>, dim3(unsigned(num_tiles)), dim3(kAttnThreads), 0, s,
-                       qp, kp, vp, block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch,
-                       num_q_heads, num_kv_heads, group, per_tile, num_blocks, c_log2, op);
-  else
-    hipLaunchKernelGGL(suffix_prefill_attn_kernel<64>, dim3(unsigned(num_tiles)), dim3(kAttnThreads), 0, s,
-                       qp, kp, vp, block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch,
-                       num_q_heads, num_kv_heads, group, per_tile, num_blocks, c_log2, op);
+  if (sh.rows == 0 || num_tiles == 0) return cw::ok();
+  launch_attn<false>(head_dim, unsigned(num_tiles), static_cast<hipStream_t>(stream), q, k_cache, v_cache,
+                     block_table, bt_stride, cu_suffix_dev, prefix_len_dev, plan_dev, batch, num_q_heads,
+                     num_kv_heads, sh, num_blocks, softmax_scale, out, 1, num_tiles, 0, nullptr, nullptr);
   return check_launch("suffix_prefill_attn launch");
+}
+
+extern "C" int64_t cw_suffix_prefill_split_workspace_bytes(int64_t total_rows, int32_t num_q_heads,
+                                                           int32_t head_dim, int32_t num_splits) {
+  if (total_rows < 0 || num_q_heads < 1 || (head_dim != 64 && head_dim != 128) || num_splits < 1 ||
+      num_splits > kMaxSplits)
+    return cw::fail(CW_EINVAL, "suffix_prefill_split_workspace_bytes: invalid argument");
+  const int64_t part_rows = total_rows * num_q_heads;
+  return split_lse_offset(part_rows, head_dim, num_splits) + int64_t(num_splits) * part_rows * 4;
+}
+
+extern "C" cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_cache, const void* v_cache,
+                                                  const int32_t* block_table, int32_t bt_stride,
+                                                  const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
+                                                  const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                                  int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                                  int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                                                  float softmax_scale, const int32_t* plan_dev,
+                                                  int32_t num_tiles, int32_t num_splits, void* workspace,
+                                                  int64_t workspace_bytes, void* out, void* stream) {
+  AttnShape sh;
+  cw_status st = check_attn("suffix_prefill_attn_split", q, k_cache, v_cache, block_table, bt_stride,
+                            cu_suffix_dev, prefix_len_dev, cu_suffix_host, prefix_len_host, batch, num_q_heads,
+                            num_kv_heads, head_dim, block_size, num_blocks, softmax_scale, plan_dev, num_tiles,
+                            out, &sh);
+  if (st != CW_OK) return st;
+  if (num_splits < 1 || num_splits > kMaxSplits)
+    return cw::fail(CW_EINVAL, "suffix_prefill_attn_split: num_splits must be in [1, 64]");
+  if (int64_t(num_tiles) * num_splits > INT32_MAX)
+    return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn_split: too many workgroups");
+  const int64_t part_rows = sh.rows * num_q_heads;
+  const int64_t need = cw_suffix_prefill_split_workspace_bytes(sh.rows, num_q_heads, head_dim, num_splits);
+  if (!workspace || workspace_bytes < need)
+    return cw::fail(CW_EINVAL, "suffix_prefill_attn_split: workspace must hold " + std::to_string(need) + " bytes");
+  if (sh.rows == 0 || num_tiles == 0) return cw::ok();
+  auto* s = static_cast<hipStream_t>(stream);
+  auto* part_o = static_cast<float*>(workspace);
+  auto* part_lse = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
+                                            split_lse_offset(part_rows, head_dim, num_splits));
+  launch_attn<true>(head_dim, unsigned(int64_t(num_tiles) * num_splits), s, q, k_cache, v_cache, block_table,
+                    bt_stride, cu_suffix_dev, prefix_len_dev, plan_dev, batch, num_q_heads, num_kv_heads, sh,
+                    num_blocks, softmax_scale, out, num_splits, num_tiles, part_rows, part_o, part_lse);
+  st = check_launch("suffix_prefill_attn_split launch");
+  if (st != CW_OK) return st;
+  return launch_merge(part_o, part_lse, num_splits, part_rows, head_dim, out, s);
+}
+
+extern "C" cw_status cw_lse_merge(const void* partial_o, const void* partial_lse, int32_t num_parts,
+                                  int64_t rows, int32_t head_dim, void* out, void* stream) {
+  if (!partial_o || !partial_lse || !out) return cw::fail(CW_EINVAL, "lse_merge: a required pointer is NULL");
+  if (num_parts < 1) return cw::fail(CW_EINVAL, "lse_merge: num_parts must be >= 1");
+  if (rows < 0) return cw::fail(CW_EINVAL, "lse_merge: rows must be >= 0");
+  if (head_dim < 8 || head_dim % 8 != 0 || head_dim > 1024)
+    return cw::fail(CW_EUNSUPPORTED, "lse_merge: head_dim must be a multiple of 8 in [8, 1024]");
+  return launch_merge(static_cast<const float*>(partial_o), static_cast<const float*>(partial_lse), num_parts,
+                      rows, head_dim, out, static_cast<hipStream_t>(stream));
 }

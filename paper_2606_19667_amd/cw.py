@@ -69,6 +69,11 @@ def _load() -> ctypes.CDLL:
         "cw_suffix_prefill_attn": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
                                           _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _i32,
                                           _vp, _vp]),
+        "cw_suffix_prefill_split_workspace_bytes": (_i64, [_i64, _i32, _i32, _i32]),
+        "cw_suffix_prefill_attn_split": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
+                                                _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _i32,
+                                                _i32, _vp, _i64, _vp, _vp]),
+        "cw_lse_merge": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp, _vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -83,7 +88,8 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_pool_destroy", "cw_pool_clone", "cw_pool_num_free", "cw_prefix_match",
             "cw_pool_alloc", "cw_pool_commit", "cw_pool_release", "cw_schedule_batch",
             "cw_release_batch", "cw_kv_append", "cw_suffix_prefill_plan_words",
-            "cw_suffix_prefill_plan", "cw_suffix_prefill_attn")
+            "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
+            "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge")
 
 
 def lib() -> ctypes.CDLL:
@@ -330,6 +336,66 @@ def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
         meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
         k_cache.shape[0], float(softmax_scale), _dev(meta.plan, torch.int32, "plan"), meta.num_tiles,
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out
+
+
+def split_count(meta: BatchMeta, num_cus: int = 256) -> int:
+    """A split count for cw_suffix_prefill_attn_split: enough runs that the
+    batch's tiles cover every CU once (one attention workgroup fits per CU)."""
+    return max(1, min(64, num_cus // max(1, meta.num_tiles)))
+
+
+def split_workspace_bytes(meta: BatchMeta, num_splits: int) -> int:
+    n = _lib.cw_suffix_prefill_split_workspace_bytes(meta.total_rows, meta.num_q_heads, meta.head_dim, num_splits)
+    if n < 0:
+        _check(int(n))
+    return int(n)
+
+
+def suffix_prefill_attn_split(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                              softmax_scale: float, num_splits: int | None = None,
+                              workspace: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                              stream=None) -> torch.Tensor:
+    """cw_suffix_prefill_attn_split: the split-KV path; returns out [total_s, Hq, D] bf16.
+    `workspace` (uint8, device) is allocated when not given."""
+    hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
+    if num_splits is None:
+        num_splits = split_count(meta)
+    if tuple(q.shape) != (meta.total_rows, hq, D):
+        raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
+    if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+    if out is None:
+        out = torch.empty_like(q)
+    elif tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must have q's shape")
+    need = split_workspace_bytes(meta, num_splits)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(_lib.cw_suffix_prefill_attn_split(
+        _dev(q, torch.bfloat16, "q"), _dev(k_cache, torch.bfloat16, "k_cache"),
+        _dev(v_cache, torch.bfloat16, "v_cache"), _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
+        _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
+        meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
+        k_cache.shape[0], float(softmax_scale), _dev(meta.plan, torch.int32, "plan"), meta.num_tiles,
+        int(num_splits), _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out
+
+
+def lse_merge(partial_o: torch.Tensor, partial_lse: torch.Tensor, out: torch.Tensor | None = None,
+              stream=None) -> torch.Tensor:
+    """cw_lse_merge: partial_o fp32 [parts, rows, D], partial_lse fp32 [parts, rows]
+    -> out bf16 [rows, D]."""
+    if partial_o.dim() != 3 or partial_lse.dim() != 2 or tuple(partial_lse.shape) != tuple(partial_o.shape[:2]):
+        raise ValueError("partial_o must be [parts, rows, D] and partial_lse [parts, rows]")
+    parts, rows, D = partial_o.shape
+    if out is None:
+        out = torch.empty((rows, D), dtype=torch.bfloat16, device=partial_o.device)
+    elif tuple(out.shape) != (rows, D):
+        raise ValueError(f"out must be [{rows}, {D}]")
+    _check(_lib.cw_lse_merge(_dev(partial_o, torch.float32, "partial_o"), _dev(partial_lse, torch.float32, "partial_lse"),
+                             parts, rows, D, _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
 

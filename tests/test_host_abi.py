@@ -315,6 +315,48 @@ def test_device_entry_points_validate_before_launch():
     assert _append([0, 0], [16]) == cw.CW_OK
 
 
+def _split(cu, plen, splits=2, ws_bytes=None, hq=32, hkv=8, d=128, workspace=True):
+    cu_a, cu_p = _arr(cu)
+    pl_a, pl_p = _arr(plen)
+    per = max(1, cw.TILE_ROWS // max(1, hq // hkv))
+    ntiles = sum(math.ceil((cu[i + 1] - cu[i]) / per) for i in range(len(plen))) * hkv
+    if ws_bytes is None:
+        ws_bytes = max(0, cw.lib().cw_suffix_prefill_split_workspace_bytes(cu[-1], hq, d, max(1, min(splits, 64))))
+    d_ = _dummy()
+    return cw.lib().cw_suffix_prefill_attn_split(d_, d_, d_, d_, 100, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d, 16,
+                                                 100, 0.1, d_, ntiles, splits, d_ if workspace else None, ws_bytes,
+                                                 d_, None)
+
+
+def test_split_workspace_size():
+    f = cw.lib().cw_suffix_prefill_split_workspace_bytes
+    # parts of O (fp32) for every (row, head), then one fp32 log-sum-exp per (row, head)
+    n = f(100, 32, 128, 3)
+    o_bytes = 3 * 100 * 32 * 128 * 4
+    assert n == -(-o_bytes // 256) * 256 + 3 * 100 * 32 * 4
+    assert f(0, 32, 128, 1) == 0
+    assert f(10, 32, 96, 1) == cw.CW_EINVAL and f(10, 32, 128, 0) == cw.CW_EINVAL
+    assert f(10, 32, 128, 65) == cw.CW_EINVAL and f(-1, 32, 128, 1) == cw.CW_EINVAL
+
+
+def test_split_and_merge_validate_before_launch():
+    E, U = cw.CW_EINVAL, cw.CW_EUNSUPPORTED
+    assert _split([0, 10], [8]) == E                       # the same batch checks as the plain call
+    assert _split([0, 10], [0], d=96) == U
+    assert _split([0, 10], [0], splits=0) == E
+    assert _split([0, 10], [0], splits=65) == E
+    assert _split([0, 10], [0], ws_bytes=16) == E          # workspace too small
+    assert "workspace" in cw.last_error()
+    assert _split([0, 10], [0], workspace=False) == E
+    d_ = _dummy()
+    merge = cw.lib().cw_lse_merge
+    assert merge(d_, d_, 0, 10, 128, d_, None) == E
+    assert merge(None, d_, 2, 10, 128, d_, None) == E
+    assert merge(d_, d_, 2, -1, 128, d_, None) == E
+    assert merge(d_, d_, 2, 10, 12, d_, None) == U
+    assert merge(d_, d_, 2, 0, 128, d_, None) == cw.CW_OK   # no rows: no launch
+
+
 def test_host_calls_reject_bad_arguments():
     with pytest.raises(cw.CwError):
         cw.Pool(0)

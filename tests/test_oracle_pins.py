@@ -167,6 +167,73 @@ def test_empty_suffix():
     assert out.shape == (0, 4, 8)
 
 
+# ---------------------------------------------------------------- partial attention + merge
+def _rand_qkv(rng, S, P, Hq, Hkv, D):
+    return (rng.standard_normal((S, Hq, D)), rng.standard_normal((P + S, Hkv, D)),
+            rng.standard_normal((P + S, Hkv, D)))
+
+
+def _merge_parts(parts, S, Hq, D):
+    o = np.stack([p[0].reshape(S * Hq, D) for p in parts])
+    l = np.stack([p[1].reshape(S * Hq) for p in parts])
+    return A.lse_merge(o, l).reshape(S, Hq, D)
+
+
+@pytest.mark.parametrize("cuts", [[0, 64], [0, 3, 64], [0, 16, 17, 40, 64], [0, 30, 35, 64]])
+def test_merge_of_key_partition_equals_full_attention(cuts):
+    """Parts over disjoint key ranges that cover all keys merge to the full
+    result; ranges past some rows' causal limit (empty parts) included."""
+    rng = np.random.default_rng(len(cuts))
+    S, P, Hq, Hkv, D = 10, 22, 4, 2, 8
+    cuts = [min(c, P + S) for c in cuts]
+    q, k, v = _rand_qkv(rng, S, P, Hq, Hkv, D)
+    parts = [A.suffix_prefill_partial(q, k, v, P, 0.2, a, b) for a, b in zip(cuts[:-1], cuts[1:])]
+    full = A.suffix_prefill_attention(q, k, v, P, 0.2)
+    assert np.abs(_merge_parts(parts, S, Hq, D) - full).max() < 1e-12
+    # the merge does not depend on the order of the parts
+    assert np.abs(_merge_parts(parts[::-1], S, Hq, D) - full).max() < 1e-12
+
+
+def test_single_part_is_full_attention_and_its_lse():
+    """One part over every key: o is the full result and lse2 is the library
+    log-sum-exp of the visible scaled scores, divided by ln 2."""
+    from scipy.special import logsumexp
+    rng = np.random.default_rng(3)
+    S, P, Hq, Hkv, D = 5, 7, 2, 1, 4
+    q, k, v = _rand_qkv(rng, S, P, Hq, Hkv, D)
+    o, lse2 = A.suffix_prefill_partial(q, k, v, P, 0.5, 0, P + S)
+    assert np.abs(o - A.suffix_prefill_attention(q, k, v, P, 0.5)).max() < 1e-12
+    for i in range(S):
+        for h in range(Hq):
+            s = 0.5 * (k[:P + i + 1, 0, :] @ q[i, h, :])
+            assert abs(lse2[i, h] - logsumexp(s) / math.log(2.0)) < 1e-12
+
+
+def test_merge_two_keys_closed_form():
+    s0, s1 = 0.7, -1.9
+    v0, v1 = np.array([[1.0, -2.0]]), np.array([[3.0, 0.5]])
+    lse = np.array([[s0 / math.log(2.0)], [s1 / math.log(2.0)]])
+    got = A.lse_merge(np.stack([v0, v1]), lse)
+    want = (math.exp(s0) * v0 + math.exp(s1) * v1) / (math.exp(s0) + math.exp(s1))
+    assert np.abs(got - want).max() < 1e-14
+
+
+def test_merge_skips_empty_parts_and_zeroes_empty_rows():
+    o = np.array([[[1.0, 2.0], [5.0, 5.0]], [[9.0, 9.0], [7.0, 8.0]]])   # [2 parts, 2 rows, 2]
+    lse = np.array([[3.0, -np.inf], [-np.inf, -np.inf]])
+    got = A.lse_merge(o, lse)
+    assert got[0].tolist() == [1.0, 2.0] and got[1].tolist() == [0.0, 0.0]
+
+
+def test_partial_rows_past_the_part_are_empty():
+    rng = np.random.default_rng(4)
+    S, P = 4, 8
+    q, k, v = _rand_qkv(rng, S, P, 2, 1, 4)
+    o, lse2 = A.suffix_prefill_partial(q, k, v, P, 0.3, P + 2, P + S)   # keys P+2 .. P+3
+    assert np.isneginf(lse2[:2]).all() and (o[:2] == 0).all()          # rows 0, 1 see none
+    assert np.isfinite(lse2[2:]).all()
+
+
 def test_flop_count_closed_form():
     # S = 2, P = 3: pairs = 2 * 3 + 3 = 9 (row 0 sees 4 keys, row 1 sees 5)
     assert A.attention_flops([3], [2], 1, 1) == 4 * 9
