@@ -241,9 +241,14 @@ def main() -> int:
     ap.add_argument("--workload", default="llama8b-trace-b16")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-diagnostic", action="store_true",
+                    help="skip the question-only diagnostic point (keeps profiler passes to one workload)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this size (counter calibration)")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        print("bench.py needs --steps >= 1 and --warmup >= 0", file=sys.stderr)
+        return 2
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(requests, KV heads or prefix blocks would be sharded across GPUs; "
@@ -298,7 +303,7 @@ def main() -> int:
         rn.bind(db.q, db.k_new, db.v_new, db.k_cache, db.v_cache, out, w.scale, stream=stream)
         rn.ev = None
         runners.append(rn)
-    def step(i: int):
+    def step(i: int, ev=None):
         rn = runners[i % 2]
         if rn.ev is not None:
             rn.ev.synchronize()
@@ -311,8 +316,15 @@ def main() -> int:
         rn.upload()
         rn.ev = torch.cuda.Event()
         rn.ev.record(stream)
-        rn.kv_append()
-        rn.attention()
+        if ev is None:
+            rn.kv_append()
+            rn.attention()
+        else:
+            ev[0].record(stream)
+            rn.kv_append()
+            ev[1].record(stream)
+            rn.attention()
+            ev[2].record(stream)
         if pool is not None:
             rn.release(pool)
             pool.close()
@@ -332,21 +344,18 @@ def main() -> int:
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
+    # Per-kernel durations: the same K steps again, with HIP events on the
+    # launch stream around each step's kv_append and attention launches (the
+    # event records cost step time, so the wall-clock pass above has none).
+    print(f"[bench] timing {args.steps} steps with per-kernel events", file=sys.stderr, flush=True)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(args.steps + i, evs[i])
+    torch.cuda.synchronize()
+    app_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    attn_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
 
-    # Per-kernel durations: the same launches back to back on the same stream,
-    # bracketed by HIP events (the schedule of the last step stays uploaded).
-    def kernel_ms(fn, n):
-        fn()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(n):
-            fn()
-        b.record(stream)
-        b.synchronize()
-        return a.elapsed_time(b) / n
-    rn = runners[(args.warmup + args.steps - 1) % 2] if args.steps else runners[0]
-    attn_ms = kernel_ms(rn.attention, max(args.steps, 10))
-    app_ms = kernel_ms(rn.kv_append, max(args.steps, 10))
+    rn = runners[(2 * args.steps - 1) % 2]
     print("[bench] per-call, cold-cache and host timings", file=sys.stderr, flush=True)
     # Per-call durations (hot caches) and with a 512 MB scratch buffer written
     # between calls, which evicts the K/V from L2 and the 256 MB MALL.
@@ -383,7 +392,7 @@ def main() -> int:
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": counted_traffic(args.workload),
-                     "kernel": "suffix_prefill_attn_kernel<128>",
+                     "kernel": "suffix_prefill_attn_kernel<128, false>",
                      "algorithmic_bytes": int(attention_bytes(P, S, hq, hkv, D))},
         "attention_call_us": hot,
         "attention_cold_us": cold,
@@ -392,7 +401,7 @@ def main() -> int:
         res["host"] = host
     del db, runners, out
     torch.cuda.empty_cache()
-    if args.workload == "llama8b-trace-b16":
+    if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
         print("[bench] question-only diagnostic point", file=sys.stderr, flush=True)
         res["diagnostic_question_only"] = question_only_point(args.seed, stream)
         torch.cuda.empty_cache()
