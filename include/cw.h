@@ -162,6 +162,61 @@ cw_status cw_release_batch(cw_pool* pool, const int32_t* block_table, int32_t bt
                            int32_t block_size);
 
 /* ------------------------------------------------------------------------
+ * Host: knowledge tree and evidence ordering (paper Sec. 3.2-3.4, Eq. 1,
+ * Algorithm 1; baselines of Sec. 4 and Table `baselines`).
+ *
+ * The tree records the document orders of served requests as root-to-node
+ * paths. A node is cached when an order inserted within the last `window`
+ * insertions passed through it and it was not marked stale since (recency
+ * stands in for residency, Sec. 3.4). l(O, T) is the number of leading
+ * documents of O whose nodes are all cached. Documents are int64 IDs; a
+ * retrieved set is given in retrieval rank and must hold distinct IDs (at
+ * most 4096). The tree is host memory owned by the library; calls on one tree
+ * are not thread-safe.
+ * ------------------------------------------------------------------------ */
+typedef struct cw_tree cw_tree;
+
+#define CW_ORDER_RETRIEVAL 0  /* retrieval rank unchanged */
+#define CW_ORDER_SORTED 1     /* lexicographic (ascending) document IDs */
+#define CW_ORDER_RECENCY 2    /* documents served within the window first, latest
+                                 first (ties in retrieval rank), then the rest in
+                                 retrieval rank */
+#define CW_ORDER_GREEDY 3     /* Algorithm 1: walk from the root, placing the first
+                                 remaining document (in retrieval rank) whose child
+                                 is cached; then the rest in retrieval rank */
+#define CW_ORDER_EXHAUSTIVE 4 /* Eq. 1: an order of maximal l(O, T); among equally
+                                 deep reused runs the one first in lexicographic
+                                 order of retrieval ranks; then the rest in
+                                 retrieval rank */
+
+/* Creates an empty tree with recency window `window` >= 1 (in insertions).
+ * CW_EINVAL: out NULL or window < 1. */
+cw_status cw_tree_create(int32_t window, cw_tree** out);
+void cw_tree_destroy(cw_tree* tree);
+/* Nodes held (excluding the root); bounded by about 2 * window * k. -1 for NULL. */
+int64_t cw_tree_num_nodes(const cw_tree* tree);
+
+/* Records a served order (Sec. 3.2: insert after serving): advances the clock
+ * by one and refreshes every node of the path. CW_EINVAL: tree NULL, k
+ * outside [0, 4096], order NULL with k > 0, repeated IDs. */
+cw_status cw_tree_insert(cw_tree* tree, const int64_t* order, int32_t k);
+
+/* Feedback (Sec. 3.4): the engine reused only `observed_depth` documents of
+ * `order`, so the nodes of `order` deeper than that are stale until an order
+ * through them is inserted again. Nodes that do not exist are skipped.
+ * CW_EINVAL as for cw_tree_insert, or observed_depth outside [0, k]. */
+cw_status cw_tree_mark_stale(cw_tree* tree, const int64_t* order, int32_t k, int32_t observed_depth);
+
+/* Orders the retrieved set `docs` [k] with `strategy` (CW_ORDER_*), writing the
+ * permutation to out_order [k]. *out_depth = l(out_order, T). *out_probes =
+ * child lookups made (Algorithm 1: at most k (k + 1) / 2). out_depth and
+ * out_probes may be NULL. The tree is not modified.
+ * CW_EINVAL: tree NULL, k outside [0, 4096], NULL arrays with k > 0, repeated
+ * IDs, unknown strategy. */
+cw_status cw_tree_order(const cw_tree* tree, int32_t strategy, const int64_t* docs, int32_t k,
+                        int64_t* out_order, int32_t* out_depth, int32_t* out_probes);
+
+/* ------------------------------------------------------------------------
  * Device: write each request's suffix K and V into its cache blocks (paper
  * Sec. 2.1: KV memory managed in fixed-size blocks).
  *

@@ -74,6 +74,12 @@ def _load() -> ctypes.CDLL:
                                                 _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _i32,
                                                 _i32, _vp, _i64, _vp, _vp]),
         "cw_lse_merge": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp, _vp]),
+        "cw_tree_create": (_i32, [_i32, ctypes.POINTER(_vp)]),
+        "cw_tree_destroy": (None, [_vp]),
+        "cw_tree_num_nodes": (_i64, [_vp]),
+        "cw_tree_insert": (_i32, [_vp, _pi64, _i32]),
+        "cw_tree_mark_stale": (_i32, [_vp, _pi64, _i32, _i32]),
+        "cw_tree_order": (_i32, [_vp, _i32, _pi64, _i32, _pi64, _pi32, _pi32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -89,7 +95,9 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_pool_alloc", "cw_pool_commit", "cw_pool_release", "cw_schedule_batch",
             "cw_release_batch", "cw_kv_append", "cw_suffix_prefill_plan_words",
             "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
-            "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge")
+            "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge",
+            "cw_tree_create", "cw_tree_destroy", "cw_tree_num_nodes", "cw_tree_insert",
+            "cw_tree_mark_stale", "cw_tree_order")
 
 
 def lib() -> ctypes.CDLL:
@@ -189,6 +197,62 @@ class Pool:
     def release(self, block_ids) -> None:
         ids = _i32_array(block_ids, "block_ids")
         _check(_lib.cw_pool_release(self._h, _ptr(ids, ctypes.c_int32), len(ids)))
+
+
+ORDER_RETRIEVAL, ORDER_SORTED, ORDER_RECENCY, ORDER_GREEDY, ORDER_EXHAUSTIVE = 0, 1, 2, 3, 4
+ORDER_NAMES = {"retrieval": ORDER_RETRIEVAL, "sorted": ORDER_SORTED, "recency": ORDER_RECENCY,
+               "greedy": ORDER_GREEDY, "exhaustive": ORDER_EXHAUSTIVE}
+
+
+def _docs_array(docs) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(list(docs), dtype=np.int64).reshape(-1))
+
+
+class KnowledgeTree:
+    """Owner of a cw_tree handle: the trie of recently served document orders
+    with the greedy walk, the exhaustive argmax and the baseline orders."""
+
+    def __init__(self, window: int = 32):
+        h = _vp()
+        _check(_lib.cw_tree_create(int(window), ctypes.byref(h)))
+        self._h = h
+        self.window = int(window)
+
+    def close(self) -> None:
+        if self._h is not None and self._h.value:
+            _lib.cw_tree_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def insert(self, order) -> None:
+        """Record a served order."""
+        a = _docs_array(order)
+        _check(_lib.cw_tree_insert(self._h, _ptr(a, ctypes.c_int64), len(a)))
+
+    def mark_stale(self, order, observed_depth: int) -> None:
+        """Mark the nodes of `order` deeper than `observed_depth` stale."""
+        a = _docs_array(order)
+        _check(_lib.cw_tree_mark_stale(self._h, _ptr(a, ctypes.c_int64), len(a), int(observed_depth)))
+
+    def order(self, docs, strategy=ORDER_GREEDY):
+        """Returns (order, depth, probes) for the retrieved set `docs` (in
+        retrieval rank); strategy is a CW_ORDER_* value or its name."""
+        if isinstance(strategy, str):
+            strategy = ORDER_NAMES[strategy]
+        a = _docs_array(docs)
+        out = np.zeros(len(a), dtype=np.int64)
+        depth, probes = ctypes.c_int32(0), ctypes.c_int32(0)
+        _check(_lib.cw_tree_order(self._h, int(strategy), _ptr(a, ctypes.c_int64), len(a),
+                                  _ptr(out, ctypes.c_int64), ctypes.byref(depth), ctypes.byref(probes)))
+        return [int(x) for x in out], depth.value, probes.value
+
+    def num_nodes(self) -> int:
+        return int(_lib.cw_tree_num_nodes(self._h))
 
 
 def schedule_batch(pool: Pool, prompts, bt_stride: int, block_size: int = BLOCK_SIZE):

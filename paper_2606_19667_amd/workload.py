@@ -3,9 +3,10 @@
 The ordering side of CacheWeaver only decides which prefix of each prompt is
 already cached; this module reproduces that shaping on the host:
 
-* `KnowledgeTree` is the trie of recently served document orders (paper
-  Sec. 3.2) with the greedy cache-aware walk (Sec. 3.3, Algorithm 1) and
-  recency as the residency estimate (Sec. 3.4).
+* The library's knowledge tree (`cw.KnowledgeTree`: the trie of recently
+  served document orders, Sec. 3.2, with the greedy walk of Sec. 3.3,
+  Algorithm 1, and recency as the residency estimate, Sec. 3.4) orders each
+  query of a trace.
 * `synthetic_trace` draws retrieved top-k sets in which consecutive queries
   share evidence (Sec. 4, workload paragraph: bursty overlapping retrieval; the
   exact generator is not given, so the sharing model is a stated choice).
@@ -24,7 +25,7 @@ from dataclasses import dataclass, field
 import numpy as np
 import torch
 
-from . import inputs
+from . import cw, inputs
 
 INSTR_TOKENS = 64
 QUESTION_TOKENS = 64
@@ -37,94 +38,8 @@ TAG_TOK, TAG_K, TAG_V, TAG_Q, TAG_TRACE, TAG_PLACE = 1, 2, 3, 4, 5, 6
 
 
 # --------------------------------------------------------------------------
-# Knowledge tree and greedy ordering
+# Retrieved sets of a synthetic trace
 # --------------------------------------------------------------------------
-class _Node:
-    __slots__ = ("children", "last_served")
-
-    def __init__(self):
-        self.children = {}
-        self.last_served = 0
-
-
-class KnowledgeTree:
-    """Trie whose root-to-node paths are document orders served recently.
-
-    A node counts as cached when some order served within the last `window`
-    insertions passed through it (recency stands in for residency, which the
-    engine controls). Nodes that fell out of the window are pruned, which keeps
-    the tree at O(window * k) nodes.
-    """
-
-    def __init__(self, window: int = 32):
-        self.window = int(window)
-        self.root = _Node()
-        self.clock = 0
-
-    def insert(self, order) -> None:
-        """Record an order after its request was served."""
-        self.clock += 1
-        node = self.root
-        for d in order:
-            child = node.children.get(d)
-            if child is None:
-                child = node.children[d] = _Node()
-            child.last_served = self.clock
-            node = child
-        if self.clock % self.window == 0:
-            self._prune(self.root)
-
-    def is_cached(self, node: _Node) -> bool:
-        return node.last_served > self.clock - self.window
-
-    def _prune(self, node: _Node) -> None:
-        for d in list(node.children):
-            c = node.children[d]
-            if not self.is_cached(c):
-                del node.children[d]
-            else:
-                self._prune(c)
-
-    def order(self, docs):
-        """Greedy cache-aware order of `docs` (given in retrieval rank).
-
-        From the root, place next the first remaining document (in retrieval
-        rank) whose child node is cached; when no remaining document extends a
-        cached path, append the rest in retrieval rank. Returns (order, depth,
-        probes): depth is the number of documents placed along cached nodes and
-        probes counts child lookups (at most k (k + 1) / 2).
-        """
-        remaining = list(docs)
-        out = []
-        node = self.root
-        probes = 0
-        depth = 0
-        while remaining:
-            nxt = None
-            for d in remaining:
-                probes += 1
-                c = node.children.get(d)
-                if c is not None and self.is_cached(c):
-                    nxt = (d, c)
-                    break
-            if nxt is None:
-                out.extend(remaining)
-                break
-            out.append(nxt[0])
-            remaining.remove(nxt[0])
-            node = nxt[1]
-            depth += 1
-        return out, depth, probes
-
-    def num_nodes(self) -> int:
-        stack, n = [self.root], 0
-        while stack:
-            x = stack.pop()
-            n += len(x.children)
-            stack.extend(x.children.values())
-        return n
-
-
 def synthetic_trace(n_queries: int, pool_size: int = 200, k: int = 5, shared: int = 3,
                     seed: int = 0):
     """Retrieved sets (each in retrieval rank) of consecutive queries.
@@ -289,7 +204,7 @@ def question_only(seed: int = 0, batch: int = 16) -> Workload:
                     seed=seed, prefix_lens=[P] * batch, free_order_key=(64,))
 
 
-def serve_trace(queries, tree: KnowledgeTree, chunk_tokens: int, uid0: int = 0):
+def serve_trace(queries, tree: "cw.KnowledgeTree", chunk_tokens: int, uid0: int = 0):
     """Order each query with the tree, insert it after serving; returns prompts
     and the greedy depth (documents) of each."""
     prompts, depths = [], []
@@ -309,7 +224,7 @@ def llama8b_trace_batch(seed: int = 0, batch: int = 16, warmup: int = 64,
     ordered by the greedy tree walk, after `warmup` served queries; 8B-shaped
     heads. Cached depths follow from prefix matching the pool."""
     qs = synthetic_trace(warmup + batch, pool_size, k, shared, seed)
-    tree = KnowledgeTree(window)
+    tree = cw.KnowledgeTree(window)
     prompts, depths = serve_trace(qs, tree, chunk_tokens)
     return Workload(f"llama8b-trace-b{batch}-k{k}-share{shared}of{k}", 32, 8, 128, 16,
                     prompts[warmup:], seed=seed, content="blocks",
