@@ -136,15 +136,50 @@ def host_timing(w, snapshot, stride: int, reps: int = 20):
         pool.close()
     res = {"schedule_us_per_request": round(best * 1e6 / w.batch, 2)}
     if w.warmup:
-        qs = W.synthetic_trace(len(w.warmup) + w.batch, seed=w.seed)
-        tree = cw.KnowledgeTree()
-        t0 = time.perf_counter()
-        for docs in qs:
-            order, _, _ = tree.order(docs)
-            tree.insert(order)
-        res["ordering_us_per_request"] = round((time.perf_counter() - t0) * 1e6 / len(qs), 2)
-        res["ordering_impl"] = "C++ knowledge tree (cw_tree_order greedy + cw_tree_insert), called from Python"
+        # The trace's queries through cw_tree_order (greedy) + cw_tree_insert,
+        # called with prepared arrays so the figure is the library's cost plus
+        # one ctypes call each.
+        import ctypes
+        qs = [np.asarray(q, dtype=np.int64) for q in W.synthetic_trace(len(w.warmup) + w.batch, seed=w.seed)]
+        lib = cw.lib()
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        outs = [np.zeros(len(q), dtype=np.int64) for q in qs]
+        args = [(q.ctypes.data_as(i64p), len(q), o.ctypes.data_as(i64p)) for q, o in zip(qs, outs)]
+        depth, probes = ctypes.c_int32(0), ctypes.c_int32(0)
+        best = float("inf")
+        for _ in range(reps):
+            tree = cw.KnowledgeTree()
+            h = tree._h
+            t0 = time.perf_counter()
+            for qp, k, op in args:
+                lib.cw_tree_order(h, cw.ORDER_GREEDY, qp, k, op, ctypes.byref(depth), ctypes.byref(probes))
+                lib.cw_tree_insert(h, op, k)
+            best = min(best, time.perf_counter() - t0)
+            tree.close()
+        res["ordering_us_per_request"] = round(best * 1e6 / len(qs), 2)
+        res["ordering_impl"] = "libcw knowledge tree: cw_tree_order (greedy) + cw_tree_insert per query"
     return res
+
+
+def ordering_point(seed: int) -> dict:
+    """The ordering side on a 200-query trace of the measured workload's
+    generator (200 chunks of 256 tokens, top-5, 3 of 5 shared): the
+    prefill-saved proxy (cached prompt tokens / prompt tokens) of each
+    ordering strategy with an unbounded pool, and of the greedy walk with and
+    without stale-path feedback when the pool holds only a few prompts. The
+    first 5 queries are warm-up."""
+    from paper_2606_19667_amd import replay as R
+    from paper_2606_19667_amd import workload as W
+    qs = W.synthetic_trace(200, pool_size=200, k=5, shared=3, seed=seed)
+    out = {"trace": "200 queries, 200 chunks x 256 tokens, top-5, 3 of 5 shared, window 32; "
+                    "first 5 queries are warm-up", "strategies": {}, "tight_pool": {}}
+    for s in ("retrieval", "sorted", "recency", "greedy", "exhaustive"):
+        out["strategies"][s] = R.replay(qs, s, seed=seed).summary(skip=5)
+    for prompts in (4, 8, 16):
+        for fb in (False, True):
+            rec = R.replay(qs, "greedy", num_blocks=prompts * 88, feedback=fb, seed=seed)
+            out["tight_pool"][f"{prompts}_prompts" + ("_feedback" if fb else "")] = rec.summary(skip=5)
+    return out
 
 
 def question_only_point(seed: int, stream):
@@ -405,6 +440,9 @@ def main() -> int:
         print("[bench] question-only diagnostic point", file=sys.stderr, flush=True)
         res["diagnostic_question_only"] = question_only_point(args.seed, stream)
         torch.cuda.empty_cache()
+    if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
+        print("[bench] ordering strategies and tight-pool replay (host)", file=sys.stderr, flush=True)
+        res["ordering"] = ordering_point(args.seed)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, sched)
