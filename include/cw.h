@@ -338,6 +338,18 @@ cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_cache, const
 cw_status cw_lse_merge(const void* partial_o, const void* partial_lse, int32_t num_parts, int64_t rows,
                        int32_t head_dim, void* out, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Host: rotary-embedding table for the suffix QKV projection. With a reused
+ * prefix only the suffix tokens are prefilled (paper Sec. 1 and 2.1), and
+ * their queries and keys are rotated at their absolute positions P_r + i (the
+ * rotate-half rotary embedding of the decoder-only models of Sec. 4).
+ *   out  host fp32 [n_positions, head_dim / 2, 2]: entry (p, j) holds
+ *        cos(p * theta_j) and sin(p * theta_j), theta_j = base^(-2 j / head_dim),
+ *        each evaluated in double precision and rounded once to fp32.
+ * CW_EINVAL: n_positions < 0, head_dim odd or outside [2, 1024], base not
+ * finite or <= 1, out NULL with n_positions > 0. */
+cw_status cw_rope_table(int32_t n_positions, int32_t head_dim, double base, float* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
-HOST_SOURCES = ["cw_host.cpp", "cw_tree.cpp"]
+HOST_SOURCES = ["cw_host.cpp", "cw_tree.cpp", "cw_proj.cpp"]
 HIP_SOURCES = ["cw_kernels.hip"]
 
 HIP_FLAGS = [

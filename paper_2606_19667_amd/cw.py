@@ -80,6 +80,7 @@ def _load() -> ctypes.CDLL:
         "cw_tree_insert": (_i32, [_vp, _pi64, _i32]),
         "cw_tree_mark_stale": (_i32, [_vp, _pi64, _i32, _i32]),
         "cw_tree_order": (_i32, [_vp, _i32, _pi64, _i32, _pi64, _pi32, _pi32]),
+        "cw_rope_table": (_i32, [_i32, _i32, ctypes.c_double, ctypes.POINTER(ctypes.c_float)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -97,7 +98,7 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
             "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge",
             "cw_tree_create", "cw_tree_destroy", "cw_tree_num_nodes", "cw_tree_insert",
-            "cw_tree_mark_stale", "cw_tree_order")
+            "cw_tree_mark_stale", "cw_tree_order", "cw_rope_table")
 
 
 def lib() -> ctypes.CDLL:
@@ -253,6 +254,14 @@ class KnowledgeTree:
 
     def num_nodes(self) -> int:
         return int(_lib.cw_tree_num_nodes(self._h))
+
+
+def rope_table(n_positions: int, head_dim: int, base: float) -> np.ndarray:
+    """cos/sin of p * theta_j for p < n_positions, j < head_dim / 2: fp32 [n, D/2, 2]."""
+    out = np.empty((max(int(n_positions), 0), int(head_dim) // 2, 2), dtype=np.float32)
+    _check(_lib.cw_rope_table(int(n_positions), int(head_dim), float(base),
+                              out.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+    return out
 
 
 def schedule_batch(pool: Pool, prompts, bt_stride: int, block_size: int = BLOCK_SIZE):
