@@ -350,6 +350,49 @@ cw_status cw_lse_merge(const void* partial_o, const void* partial_lse, int32_t n
  * finite or <= 1, out NULL with n_positions > 0. */
 cw_status cw_rope_table(int32_t n_positions, int32_t head_dim, double base, float* out);
 
+/* ------------------------------------------------------------------------
+ * Device: suffix QKV projection with rotary embedding, fused with the KV
+ * append. With a reused prefix only the suffix tokens are prefilled (paper
+ * Sec. 1 and 2.1); per layer that starts by projecting each suffix token's
+ * hidden state to its query, key and value heads, rotating queries and keys
+ * at the token's absolute position, and storing keys and values in the
+ * request's cache blocks (Sec. 2.1). For suffix row t = cu[r] + i of request
+ * r, at position p = P_r + i:
+ *   y      = x[t] W^T (+ bias)        fp32 accumulation of bf16 products
+ *   y_q, y_k, y_v = features [0, Hq D), [Hq D, (Hq + Hkv) D), the rest
+ *   rot(u)[j]         = u[j] cos(p th_j) - u[j + D/2] sin(p th_j)
+ *   rot(u)[j + D/2]   = u[j + D/2] cos(p th_j) + u[j] sin(p th_j),  j < D/2
+ *   q_out[t][h][:]    = rot(y_q of head h)
+ *   k_cache[blk][g][p % 16][:], v_cache[blk][g][:][p % 16] = rot(y_k), y_v
+ *     of KV head g, blk = block_table[r][p / 16]; a block id outside
+ *     [0, num_blocks) is skipped (nothing written).
+ * Every output is rounded once, RNE, to bf16; every other cache byte keeps
+ * its value.
+ *   x       device bf16 [total_s, hidden], rows in request order
+ *   w       device bf16 [(Hq + 2 Hkv) head_dim, hidden] (one row per feature)
+ *   bias    device bf16 [(Hq + 2 Hkv) head_dim], or NULL for none
+ *   rope    device fp32 [rope_len, head_dim / 2, 2]: (cos, sin) of p th_j, as
+ *           cw_rope_table writes it; every suffix position must be < rope_len
+ *   hidden  multiple of 32 in [32, 2^20]
+ *   q_out   device bf16 [total_s, Hq, head_dim]
+ *   k_cache, v_cache, block_table, cu_suffix_*, prefix_len_*: as for
+ *           cw_kv_append (cu/prefix on host for validation and launch sizing,
+ *           on device for the kernel; both copies must agree)
+ * All device pointers 16-byte aligned; the caller owns every buffer. Runs
+ * asynchronously on `stream` (NULL = default stream).
+ * x and q_out may be NULL when total_s is 0 (nothing is launched).
+ * CW_EINVAL: NULL pointer (other than bias), head counts, num_blocks < 1,
+ * rope_len < 0 or too short, the batch checks of cw_kv_append.
+ * CW_EUNSUPPORTED: head_dim not 64 or 128, block_size != 16, hidden not a
+ * multiple of 32 in range, total_s too large. CW_EHIP: launch failure. */
+cw_status cw_qkv_rope_append(const void* x, const void* w, const void* bias, const float* rope,
+                             int32_t rope_len, int32_t hidden, void* q_out, void* k_cache, void* v_cache,
+                             const int32_t* block_table, int32_t bt_stride, const int32_t* cu_suffix_dev,
+                             const int32_t* prefix_len_dev, const int32_t* cu_suffix_host,
+                             const int32_t* prefix_len_host, int32_t batch, int32_t num_q_heads,
+                             int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                             void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,0 +1,347 @@
+// Device half of libcw for gfx950 (MI355X): the suffix QKV projection with
+// rotary embedding, fused with the KV append.
+//
+// Paper Sec. 1 and 2.1: a prefix hit removes every per-layer prefill step of
+// the cached tokens; for the suffix tokens the layer still projects each
+// hidden state to its query, key and value heads, rotates queries and keys by
+// their absolute position, and stores the new keys and values in the
+// request's cache blocks. This kernel does those three steps in one pass:
+//
+//   y = x W^T (+ b)          x [T, hidden], W [(Hq + 2 Hkv) D, hidden]
+//   q, k = rope(y_q, y_k)    rotate-half form at position P_r + i
+//   q -> q_out [T, Hq, D];  k -> K cache [blk][g][slot][d];
+//   v -> V cache [blk][g][d][slot] (each block stored transposed)
+//
+// Design (one workgroup = 8 wavefronts = one 256-feature x 256-token tile):
+//  * The product is formed as C^T = W x^T with v_mfma_f32_32x32x16_bf16:
+//    A = 32 rows of W, B = 32 token rows of x. In the 32x32 accumulator a
+//    lane then holds one token and 16 features, so everything the epilogue
+//    needs per element (position, block, slot) is per lane.
+//  * Wave (wf, wt) owns features {j0 .. j0 + 31} and {j0 + D/2 .. + 31} of one
+//    head and 128 tokens. The two feature blocks are exactly the rotary pairs
+//    (j, j + D/2), which therefore sit in the same lane and register of two
+//    accumulators: the rotation needs no data exchange.
+//  * Hidden is walked in steps of 32. Four LDS stages of 32 KB (W rows then x
+//    rows, 64 bytes each) are filled by LDS-direct loads (global_load_lds,
+//    no registers), three steps ahead of their use; one barrier per step.
+//    The 16-byte chunk c of LDS row r holds global chunk c ^ ((r >> 2) & 3),
+//    so the 16 rows read by one operand phase hit distinct banks.
+//  * Tiles are numbered XCD-major (workgroup b runs on XCD b % 8), and within
+//    an XCD feature tiles vary fastest in groups of 8, so the workgroups that
+//    run together on one L2 share their W and x rows.
+//  * fp32 accumulation; bias, rotation (fp32 cos/sin from a table the host
+//    computes in fp64) and one bf16 rounding in the epilogue.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <string>
+
+#include "cw_internal.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kThreads = 512;                  // 8 wavefronts
+constexpr int kTileF = 256;                    // output features per workgroup
+constexpr int kTileT = 256;                    // tokens per workgroup
+constexpr int kStep = 32;                      // hidden elements per pipeline step
+constexpr int kRow = kStep * 2;                // bytes of one staged row
+constexpr int kPart = kTileF * kRow;           // 16 KB: the W (or x) rows of a stage
+constexpr int kStage = 2 * kPart;
+constexpr int kStages = 4;
+constexpr int kAhead = kStages - 1;            // steps in flight
+constexpr int kCopies = 4;                     // 1 KB LDS-direct copies per wave and step
+constexpr int kGroupF = 8;                     // feature tiles per XCD group
+constexpr int kBs = cw::kBlockSize;
+static_assert(kTileF == kTileT, "one staging layout serves W and x");
+static_assert(kStages * kStage <= 160 * 1024, "LDS of one CU");
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
+
+// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l. (Not in
+// the kernel template: the host pass of a template that names this builtin
+// directly emits no launch stub.)
+__device__ __forceinline__ void copy16_to_lds(const void* src, lds_void_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+// s_waitcnt immediates (gfx9 encoding): vmcnt(n) with lgkmcnt(0), expcnt untouched.
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | (7 << 4) | ((n >> 4) << 14); }
+
+// Chunk swizzle of staged row r (64-byte rows, four 16-byte chunks).
+__device__ __forceinline__ int row_swz(int r) { return (r >> 2) & 3; }
+
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __restrict__ w,
+                            const uint16_t* __restrict__ bias, const float* __restrict__ rope,
+                            int T, int hidden, int n_feat, uint16_t* __restrict__ q_out,
+                            uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache,
+                            const int32_t* __restrict__ bt, int bt_stride, const int32_t* __restrict__ cu,
+                            const int32_t* __restrict__ plen, int batch, int hq, int hkv, int num_blocks,
+                            int n_ftiles, int n_ttiles, int per_xcd) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStage];
+
+  // ---- tile of this workgroup
+  const int b = blockIdx.x;
+  const int L = (b & 7) * per_xcd + (b >> 3);
+  if (L >= n_ftiles * n_ttiles) return;
+  const int grp = L / (kGroupF * n_ttiles);
+  const int gf = min(kGroupF, n_ftiles - grp * kGroupF);
+  const int rem = L - grp * kGroupF * n_ttiles;
+  const int tt = rem / gf;
+  const int ft = grp * kGroupF + rem % gf;
+  const int f0 = ft * kTileF;
+  const int t0 = tt * kTileT;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int l32 = lane & 31;
+  const int half = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // ---- staging role: W rows and x rows 32 wave .. 32 wave + 31 of each step
+  const int64_t hb = int64_t(hidden) * 2;   // bytes per row of W and x
+  const uint8_t* src[kCopies];
+#pragma unroll
+  for (int i = 0; i < kCopies; ++i) {
+    const int row = 32 * wave + 16 * (i & 1) + (lane >> 2);
+    const int chunk = (lane & 3) ^ row_swz(row);
+    const uint8_t* base = (i < 2) ? w + int64_t(min(f0 + row, n_feat - 1)) * hb
+                                  : x + int64_t(min(t0 + row, T - 1)) * hb;
+    src[i] = base + chunk * 16;
+  }
+  auto issue = [&](int step, int st) __attribute__((always_inline)) {
+    uint8_t* dst = lds + st * kStage + wave * 2048;
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i)
+      copy16_to_lds(src[i] + int64_t(step) * kRow, (lds_void_t*)(dst + (i >> 1) * kPart + (i & 1) * 1024));
+  };
+
+  // ---- operand rows of this wave
+  constexpr int kWavesPerHead = D / 64;
+  const int wf = wave & 3, wt = wave >> 2;
+  const int head_l = wf / kWavesPerHead;                 // head inside the tile
+  const int j0 = (wf % kWavesPerHead) * 32;              // first rotary index of the wave
+  const int arow0 = head_l * D + j0;                     // tile rows of the two W blocks
+  const int arow1 = arow0 + D / 2;
+  const int brow = wt * 128;                             // first tile token of the wave
+  // in-stage byte offset of slice kk for a block starting at a multiple of 32 rows
+  int sw[2];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) sw[kk] = l32 * kRow + (((2 * kk + half) ^ row_swz(l32)) << 4);
+
+  f32x16 acc0[4], acc1[4];
+#pragma unroll
+  for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc0[tb][e] = acc1[tb][e] = 0.f;
+
+  const int nk = hidden / kStep;
+#pragma unroll
+  for (int s = 0; s < kAhead; ++s)
+    if (s < nk) issue(s, s);
+
+  for (int k = 0; k < nk; ++k) {
+    // this wave's copies of step k have landed (later steps may be in flight)
+    const int later = min(nk - 1 - k, kAhead - 1);
+    if (later >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * kCopies));
+    else if (later == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kCopies));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    // stage (k + 3) % 4 was last read in step k - 1, which every wave has left
+    if (k + kAhead < nk) issue(k + kAhead, (k + kAhead) % kStages);
+
+    const uint8_t* st = lds + (k % kStages) * kStage;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const bf16x8 a0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + arow0 * kRow + sw[kk]));
+      const bf16x8 a1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + arow1 * kRow + sw[kk]));
+      bf16x8 bx[4];
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb)
+        bx[tb] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(st + kPart + (brow + 32 * tb) * kRow + sw[kk]));
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) {
+        acc0[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bx[tb], acc0[tb], 0, 0, 0);
+        acc1[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bx[tb], acc1[tb], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- epilogue: bias, rotation, bf16 rounding, stores
+  const int hf = (f0 + head_l * D) / D;   // global head index of the wave's features
+  if (hf >= hq + 2 * hkv) return;         // past the last head (partial feature tile)
+  const int kind = hf < hq ? 0 : (hf < hq + hkv ? 1 : 2);   // q, k or v
+  const int g = kind == 1 ? hf - hq : hf - hq - hkv;
+  // rotary index / head-dim offset of register e of block 0: j0 + dq(e)
+  // with dq(e) = 8 (e / 4) + 4 half + e % 4; block 1 is + D / 2.
+  float bb0[16], bb1[16];
+  if (bias) {
+    const uint16_t* bp = bias + int64_t(hf) * D + j0 + 4 * half;
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const u32x2 v0 = *reinterpret_cast<const u32x2*>(bp + 8 * q4);
+      const u32x2 v1 = *reinterpret_cast<const u32x2*>(bp + 8 * q4 + D / 2);
+      bb0[4 * q4 + 0] = bf16_lo(v0[0]); bb0[4 * q4 + 1] = bf16_hi(v0[0]);
+      bb0[4 * q4 + 2] = bf16_lo(v0[1]); bb0[4 * q4 + 3] = bf16_hi(v0[1]);
+      bb1[4 * q4 + 0] = bf16_lo(v1[0]); bb1[4 * q4 + 1] = bf16_hi(v1[0]);
+      bb1[4 * q4 + 2] = bf16_lo(v1[1]); bb1[4 * q4 + 3] = bf16_hi(v1[1]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) bb0[e] = bb1[e] = 0.f;
+  }
+
+#pragma unroll
+  for (int tb = 0; tb < 4; ++tb) {
+    const int t = t0 + brow + 32 * tb + l32;
+    if (t >= T) continue;
+    // request of token t: the largest r with cu[r] <= t
+    int lo = 0, hi = batch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (cu[mid] <= t) lo = mid;
+      else hi = mid - 1;
+    }
+    const int pos = plen[lo] + (t - cu[lo]);
+    float o0[16], o1[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      o0[e] = acc0[tb][e] + bb0[e];
+      o1[e] = acc1[tb][e] + bb1[e];
+    }
+    if (kind != 2) {
+      const float* cs = rope + (int64_t(pos) * (D / 2) + j0 + 4 * half) * 2;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const f32x4 c01 = *reinterpret_cast<const f32x4*>(cs + 16 * q4);
+        const f32x4 c23 = *reinterpret_cast<const f32x4*>(cs + 16 * q4 + 4);
+        const float c[4] = {c01[0], c01[2], c23[0], c23[2]};
+        const float s[4] = {c01[1], c01[3], c23[1], c23[3]};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float a = o0[4 * q4 + i], bv = o1[4 * q4 + i];
+          o0[4 * q4 + i] = a * c[i] - bv * s[i];
+          o1[4 * q4 + i] = bv * c[i] + a * s[i];
+        }
+      }
+    }
+    if (kind == 0) {
+      uint16_t* qp = q_out + (int64_t(t) * hq + hf) * D + j0 + 4 * half;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        *reinterpret_cast<u32x2*>(qp + 8 * q4) =
+            u32x2{pack_bf16x2(o0[4 * q4], o0[4 * q4 + 1]), pack_bf16x2(o0[4 * q4 + 2], o0[4 * q4 + 3])};
+        *reinterpret_cast<u32x2*>(qp + 8 * q4 + D / 2) =
+            u32x2{pack_bf16x2(o1[4 * q4], o1[4 * q4 + 1]), pack_bf16x2(o1[4 * q4 + 2], o1[4 * q4 + 3])};
+      }
+      continue;
+    }
+    const int blk = bt[int64_t(lo) * bt_stride + pos / kBs];
+    if (blk < 0 || blk >= num_blocks) continue;
+    const int slot = pos % kBs;
+    if (kind == 1) {
+      uint16_t* kp = k_cache + ((int64_t(blk) * hkv + g) * kBs + slot) * D + j0 + 4 * half;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        *reinterpret_cast<u32x2*>(kp + 8 * q4) =
+            u32x2{pack_bf16x2(o0[4 * q4], o0[4 * q4 + 1]), pack_bf16x2(o0[4 * q4 + 2], o0[4 * q4 + 3])};
+        *reinterpret_cast<u32x2*>(kp + 8 * q4 + D / 2) =
+            u32x2{pack_bf16x2(o1[4 * q4], o1[4 * q4 + 1]), pack_bf16x2(o1[4 * q4 + 2], o1[4 * q4 + 3])};
+      }
+    } else {
+      uint16_t* vp = v_cache + ((int64_t(blk) * hkv + g) * D + j0 + 4 * half) * kBs + slot;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = 8 * q4 + i;
+          vp[d * kBs] = uint16_t(pack_bf16x2(o0[4 * q4 + i], 0.f));
+          vp[(d + D / 2) * kBs] = uint16_t(pack_bf16x2(o1[4 * q4 + i], 0.f));
+        }
+    }
+  }
+}
+
+cw_status check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return cw::fail(CW_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+  return cw::ok();
+}
+
+}  // namespace
+
+extern "C" cw_status cw_qkv_rope_append(const void* x, const void* w, const void* bias, const float* rope,
+                                        int32_t rope_len, int32_t hidden, void* q_out, void* k_cache,
+                                        void* v_cache, const int32_t* block_table, int32_t bt_stride,
+                                        const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
+                                        const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                        int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                        int32_t head_dim, int32_t block_size, int32_t num_blocks, void* stream) {
+  const char* what = "qkv_rope_append";
+  if (!w || !rope || !k_cache || !v_cache || !block_table || !cu_suffix_dev || !prefix_len_dev)
+    return cw::fail(CW_EINVAL, std::string(what) + ": a required pointer is NULL");
+  if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0)
+    return cw::fail(CW_EINVAL, std::string(what) + ": num_q_heads must be a positive multiple of num_kv_heads");
+  if (num_blocks < 1) return cw::fail(CW_EINVAL, std::string(what) + ": num_blocks must be >= 1");
+  if (head_dim != 64 && head_dim != 128)
+    return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": head_dim must be 64 or 128");
+  if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": block_size must be 16");
+  if (hidden < kStep || hidden % kStep != 0 || hidden > (1 << 20))
+    return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": hidden must be a multiple of 32 in [32, 2^20]");
+  if (rope_len < 0) return cw::fail(CW_EINVAL, std::string(what) + ": rope_len must be >= 0");
+  int64_t rows = 0;
+  cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &rows);
+  if (st != CW_OK) return st;
+  int64_t max_pos = -1;   // largest position of a suffix row
+  for (int32_t r = 0; r < batch; ++r)
+    if (cu_suffix_host[r + 1] > cu_suffix_host[r])
+      max_pos = std::max<int64_t>(max_pos, int64_t(prefix_len_host[r]) + cu_suffix_host[r + 1] - cu_suffix_host[r] - 1);
+  if (max_pos >= rope_len)
+    return cw::fail(CW_EINVAL, std::string(what) + ": the rotary table holds " + std::to_string(rope_len) +
+                                   " positions, position " + std::to_string(max_pos) + " is needed");
+  if (rows == 0) return cw::ok();
+  if (!x || !q_out) return cw::fail(CW_EINVAL, std::string(what) + ": x and q_out are required");
+  if (rows > INT32_MAX - kTileT) return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": too many suffix rows");
+  const int64_t n_feat = int64_t(num_q_heads + 2 * num_kv_heads) * head_dim;
+  const int64_t n_ftiles = (n_feat + kTileF - 1) / kTileF;
+  const int64_t n_ttiles = (rows + kTileT - 1) / kTileT;
+  const int64_t per_xcd = (n_ftiles * n_ttiles + cw::kNumXcd - 1) / cw::kNumXcd;
+  if (per_xcd * cw::kNumXcd > INT32_MAX) return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": too many tiles");
+  auto* s = static_cast<hipStream_t>(stream);
+  const dim3 grid(unsigned(per_xcd * cw::kNumXcd));
+  auto* xp = static_cast<const uint8_t*>(x);
+  auto* wp = static_cast<const uint8_t*>(w);
+  auto* bp = static_cast<const uint16_t*>(bias);
+  auto* qp = static_cast<uint16_t*>(q_out);
+  auto* kp = static_cast<uint16_t*>(k_cache);
+  auto* vp = static_cast<uint16_t*>(v_cache);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(qkv_rope_append_kernel<128>, grid, dim3(kThreads), 0, s, xp, wp, bp, rope, int(rows), hidden,
+                       int(n_feat), qp, kp, vp, block_table, bt_stride, cu_suffix_dev, prefix_len_dev, batch,
+                       num_q_heads, num_kv_heads, num_blocks, int(n_ftiles), int(n_ttiles), int(per_xcd));
+  else
+    hipLaunchKernelGGL(qkv_rope_append_kernel<64>, grid, dim3(kThreads), 0, s, xp, wp, bp, rope, int(rows), hidden,
+                       int(n_feat), qp, kp, vp, block_table, bt_stride, cu_suffix_dev, prefix_len_dev, batch,
+                       num_q_heads, num_kv_heads, num_blocks, int(n_ftiles), int(n_ttiles), int(per_xcd));
+  return check_launch("qkv_rope_append launch");
+}

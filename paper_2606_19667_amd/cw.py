@@ -81,6 +81,8 @@ def _load() -> ctypes.CDLL:
         "cw_tree_mark_stale": (_i32, [_vp, _pi64, _i32, _i32]),
         "cw_tree_order": (_i32, [_vp, _i32, _pi64, _i32, _pi64, _pi32, _pi32]),
         "cw_rope_table": (_i32, [_i32, _i32, ctypes.c_double, ctypes.POINTER(ctypes.c_float)]),
+        "cw_qkv_rope_append": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
+                                      _pi32, _pi32, _i32, _i32, _i32, _i32, _i32, _i32, _vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -98,7 +100,7 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
             "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge",
             "cw_tree_create", "cw_tree_destroy", "cw_tree_num_nodes", "cw_tree_insert",
-            "cw_tree_mark_stale", "cw_tree_order", "cw_rope_table")
+            "cw_tree_mark_stale", "cw_tree_order", "cw_rope_table", "cw_qkv_rope_append")
 
 
 def lib() -> ctypes.CDLL:
@@ -388,6 +390,42 @@ def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache
                              _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
                              meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hkv, D, BLOCK_SIZE,
                              k_cache.shape[0], _stream(stream)))
+
+
+def qkv_rope_append(meta: BatchMeta, x: torch.Tensor, w: torch.Tensor, rope: torch.Tensor,
+                    k_cache: torch.Tensor, v_cache: torch.Tensor, bias: torch.Tensor | None = None,
+                    q_out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """cw_qkv_rope_append: project the suffix rows x [total_s, hidden] with w
+    [(Hq + 2 Hkv) D, hidden] (+ bias), rotate q and k at their positions with
+    the table rope [n, D/2, 2] (cw.rope_table on the device), write k and v into
+    the cache blocks and return q_out [total_s, Hq, D] bf16."""
+    hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
+    if x.dim() != 2 or x.shape[0] != meta.total_rows:
+        raise ValueError(f"x must be [{meta.total_rows}, hidden], got {tuple(x.shape)}")
+    hidden = int(x.shape[1])
+    nf = (hq + 2 * hkv) * D
+    if tuple(w.shape) != (nf, hidden):
+        raise ValueError(f"w must be [{nf}, {hidden}], got {tuple(w.shape)}")
+    if bias is not None and tuple(bias.shape) != (nf,):
+        raise ValueError(f"bias must be [{nf}], got {tuple(bias.shape)}")
+    if rope.dim() != 3 or tuple(rope.shape[1:]) != (D // 2, 2):
+        raise ValueError(f"rope must be [n, {D // 2}, 2], got {tuple(rope.shape)}")
+    if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+    if q_out is None:
+        q_out = torch.empty((meta.total_rows, hq, D), dtype=torch.bfloat16, device=x.device)
+    elif tuple(q_out.shape) != (meta.total_rows, hq, D):
+        raise ValueError(f"q_out must be [{meta.total_rows}, {hq}, {D}]")
+    _check(_lib.cw_qkv_rope_append(
+        _dev(x, torch.bfloat16, "x"), _dev(w, torch.bfloat16, "w"),
+        None if bias is None else _dev(bias, torch.bfloat16, "bias"), _dev(rope, torch.float32, "rope"),
+        int(rope.shape[0]), hidden, _dev(q_out, torch.bfloat16, "q_out"),
+        _dev(k_cache, torch.bfloat16, "k_cache"), _dev(v_cache, torch.bfloat16, "v_cache"),
+        _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
+        _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
+        meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
+        k_cache.shape[0], _stream(stream)))
+    return q_out
 
 
 def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,

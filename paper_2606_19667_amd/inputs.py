@@ -32,6 +32,15 @@ def normal_bf16(key, shape, device="cpu") -> torch.Tensor:
     return x.to(torch.bfloat16)
 
 
+def scaled_normal_bf16(key, shape, std: float, device="cpu") -> torch.Tensor:
+    """bfloat16 tensor of N(0, std^2) draws for `key`: std times an N(0, 1) draw
+    in float32, then rounded (weights of a linear layer use std = fan_in^-1/2)."""
+    g = torch.Generator(device=device)
+    g.manual_seed(_seed64(key) & ((1 << 63) - 1))
+    x = torch.randn(tuple(shape), generator=g, dtype=torch.float32, device=device)
+    return (x * float(std)).to(torch.bfloat16)
+
+
 def token_ids(key, n: int, vocab: int = VOCAB) -> np.ndarray:
     """int32 token IDs for `key`."""
     rng = np.random.default_rng(np.random.SeedSequence([int(x) for x in key]))

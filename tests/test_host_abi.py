@@ -315,6 +315,32 @@ def test_device_entry_points_validate_before_launch():
     assert _append([0, 0], [16]) == cw.CW_OK
 
 
+def _qkv(cu, plen, rope_len=4096, hidden=256, hq=8, hkv=2, d=128, bs=16, stride=100, nb=100, bias=True, x=True):
+    cu_a, cu_p = _arr(cu)
+    pl_a, pl_p = _arr(plen)
+    d_ = _dummy()
+    return cw.lib().cw_qkv_rope_append(d_ if x else None, d_, d_ if bias else None, d_, rope_len, hidden, d_, d_,
+                                       d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d, bs, nb, None)
+
+
+def test_qkv_rope_append_validates_before_launch():
+    E, U = cw.CW_EINVAL, cw.CW_EUNSUPPORTED
+    assert _qkv([0, 10], [8]) == E                        # the batch checks of the append
+    assert _qkv([0, 1000], [16 * 90]) == E
+    assert _qkv([0, 10], [0], x=False) == E
+    assert _qkv([0, 10], [0], hq=6, hkv=4) == E
+    assert _qkv([0, 10], [0], nb=0) == E
+    assert _qkv([0, 10], [0], d=96) == U
+    assert _qkv([0, 10], [0], bs=32) == U
+    assert _qkv([0, 10], [0], hidden=48) == U             # not a multiple of 32
+    assert _qkv([0, 10], [0], hidden=0) == U
+    assert _qkv([0, 10], [0], rope_len=-1) == E
+    assert _qkv([0, 10, 20], [32, 48], rope_len=57) == E  # last position 48 + 9 = 57 needs 58 entries
+    assert "rotary table" in cw.last_error()
+    assert _qkv([0, 0], [16], rope_len=0) == cw.CW_OK      # nothing to do: no launch
+    assert _qkv([0, 0, 0], [16, 32], rope_len=0, bias=False) == cw.CW_OK
+
+
 def _split(cu, plen, splits=2, ws_bytes=None, hq=32, hkv=8, d=128, workspace=True):
     cu_a, cu_p = _arr(cu)
     pl_a, pl_p = _arr(plen)
