@@ -5,23 +5,21 @@
 // suffix tokens are prefilled; they attend causally over themselves and fully
 // over the prefix, whose K/V the engine keeps in fixed-size blocks.
 //
-// Attention kernel design (one workgroup = 4 wavefronts = one tile):
-//  * A tile is (request r, KV head g, a run of T suffix rows); its 128 MFMA
-//    rows pack the G = Hq/Hkv query heads of g over T = 128/G positions, so
+// Attention kernel design (one workgroup = 8 wavefronts, two per SIMD = one tile):
+//  * A tile is (request r, KV head g, a run of T suffix rows); its 256 MFMA
+//    rows pack the G = Hq/Hkv query heads of g over T = 256/G positions, so
 //    every K/V byte staged in LDS serves all heads of the group.
 //  * Each wave owns 32 packed rows and computes S^T = K Q^T with
 //    v_mfma_f32_32x32x16_bf16: in the 32x32 accumulator layout a lane then
 //    holds one query column and 16 keys, so row max / sum need one exchange
-//    with lane ^ 32 and the softmax state (m, l, rescale) is lane-local.
-//  * O^T = V^T P^T reuses the score registers directly as the B operand (the
-//    key order inside an MFMA's 16-key slice only has to agree between A and
-//    B); V is transposed into LDS as [d][key] when it is staged.
-//  * K/V tiles of 64 keys (4 blocks) are gathered through the block table with
-//    16-byte loads (each block of one KV head is one contiguous 16 x D run),
-//    prefetched into registers while the previous tile is computed.
-//  * Softmax in fp32 with exp2 and the scale folded into one FMA; only tiles
-//    that cross the causal diagonal apply the mask; keys past the prompt end
-//    are zero-filled so stale cache bytes never reach the result.
+//    with lane ^ 32 and the softmax state is lane-local.
+//  * O^T = V^T P^T uses the packed probabilities directly as the B operand;
+//    the cache keeps each V block transposed, so V operands are plain reads.
+//  * K/V steps of 64 keys (4 blocks) are copied from the cache into a ring of
+//    three LDS stages by load-to-LDS instructions, two to three steps ahead.
+//  * Softmax in fp32 and base 2 with a lazily moved base; only steps that
+//    cross the causal diagonal apply the mask; keys past the prompt end are
+//    zero-filled so stale cache bytes never reach the result.
 
 #include <hip/hip_runtime.h>
 
@@ -199,11 +197,28 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l. (Kept
-// out of the kernel template: the host pass of a template that names this
-// builtin directly emits no launch stub.)
+// The attention kernel orders its cache copies against its LDS reads itself,
+// with explicit vmcnt waits and workgroup barriers. Its two memory helpers are
+// asm statements so that the compiler does not add waits of its own: a
+// load-to-LDS copy it can see makes it put a vmcnt(0) before LDS reads it
+// cannot tell apart from the copy's target, and a register load it can see may
+// be waited for with vmcnt(0) far from its use. Either drains every copy in
+// flight. The compiler's own vmcnt waits only become more conservative for
+// memory operations it does not see.
+
+// 16 bytes through registers, waited for at once (every older memory operation
+// of the wave completes with it). Used only for blocks that are not whole.
+__device__ __forceinline__ u32x4 load16_now(const void* src) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off\n\ts_waitcnt vmcnt(0)" : "=v"(v) : "v"(src) : "memory");
+  return v;
+}
+
+// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l. M0 holds
+// the LDS address (one wait state between writing M0 and the copy).
 __device__ __forceinline__ void copy16_to_lds(const void* src, lds_void_t* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst))) : "memory");
 }
 
 constexpr int kAttnWaves = 8;
@@ -347,7 +362,10 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   // Physical block of logical block lb, or -1 past the prompt / outside the
   // pool; the table index is clamped into the request's row (always in bounds).
   auto block_id = [&](int lb) __attribute__((always_inline)) -> int {
-    const int b = btr[min(lb, nblk - 1)];
+    // read through the constant address space: a scalar load (a vector load
+    // would be waited for with vmcnt, which also waits for the copies)
+    const int b = reinterpret_cast<const __attribute__((address_space(4))) int32_t*>(
+        reinterpret_cast<uintptr_t>(btr))[min(lb, nblk - 1)];
     return (lb < nblk && b >= 0 && b < num_blocks) ? b : -1;
   };
   // Stages step t's block of this wave into stage st; returns whether it used
@@ -366,7 +384,8 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
     const u32x4 zero{0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < LPW; ++i) {
-      u32x4 v = b >= 0 ? *reinterpret_cast<const u32x4*>(src + src_off[i]) : zero;
+      u32x4 v = zero;
+      if (b >= 0) v = load16_now(src + src_off[i]);
       if (is_v) {
         // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
         const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
@@ -417,14 +436,14 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   };
   // Causal mask of the step starting at key k0.
   auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
-    const int lim = qpos - k0;   // k0: absolute first key of the step
+    // key of element e of half h is h 32 + (e / 8) 16 + half 8 + e % 8; the
+    // lane term moves to the limit so that the per-element terms stay immediates
+    const int lim = qpos - k0 - half * 8;
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = h * 32 + (e >> 3) * 16 + half * 8 + (e & 7);
-        if (key > lim) sc[h][e] = -INFINITY;
-      }
+      for (int e = 0; e < 16; ++e)
+        if (h * 32 + (e >> 3) * 16 + (e & 7) > lim) sc[h][e] = -INFINITY;
   };
   // Maximum of the row over the step's 64 keys (this lane's 32 and lane ^ 32's).
   auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) -> float {
