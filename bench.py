@@ -224,6 +224,46 @@ def question_only_point(seed: int, stream):
     return res
 
 
+def qkv_projection_point(w, seed: int, stream, hidden: int = 4096, rope_base: float = 500000.0):
+    """The suffix QKV projection with rotary embedding, fused with the KV append
+    (cw_qkv_rope_append), on the measured batch's suffix rows: an 8B-shaped
+    layer (hidden 4096, 32 Q / 8 KV heads of 128, rope base 500000) with
+    seeded random bf16 hidden states and weights. Algorithmic FLOPs are
+    2 T hidden (Hq + 2 Hkv) D; bytes are x, W and the bf16 outputs once.
+    hipBLASLt's time for the bare product x W^T is given for context."""
+    import torch
+    from paper_2606_19667_amd import batch as B
+    from paper_2606_19667_amd import cw, inputs
+    s = B.schedule(w)
+    hq, hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
+    T = int(s.cu_suffix[-1])
+    nf = (hq + 2 * hkv) * D
+    meta = cw.BatchMeta(s.block_table, s.cu_suffix, s.prefix_len, hq, hkv, D)
+    x = inputs.normal_bf16((seed, 101), (T, hidden), "cuda")
+    wt = inputs.scaled_normal_bf16((seed, 102), (nf, hidden), hidden ** -0.5, "cuda")
+    kc = torch.zeros((s.num_blocks, hkv, 16, D), dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros((s.num_blocks, hkv, D, 16), dtype=torch.bfloat16, device="cuda")
+    n_pos = int((s.prefix_len + np.diff(s.cu_suffix)).max())
+    rope = torch.from_numpy(cw.rope_table(n_pos, D, rope_base)).cuda()
+    q = torch.empty((T, hq, D), dtype=torch.bfloat16, device="cuda")
+    fn = lambda: cw.qkv_rope_append(meta, x, wt, rope, kc, vc, q_out=q, stream=stream)
+    for _ in range(5):
+        fn()
+    t = percentiles_us(timed_calls(fn, stream, 30))
+    fl = 2.0 * T * hidden * nf
+    by = 2 * (T * hidden + nf * hidden + T * nf)
+    sec = t["median"] * 1e-6
+    gemm = lambda: x @ wt.t()
+    for _ in range(5):
+        gemm()
+    tg = percentiles_us(timed_calls(gemm, stream, 30))
+    return {"kernel": "qkv_rope_append_kernel<128>", "tokens": T, "hidden": hidden, "features": nf,
+            "us": t, "GFLOP": round(fl / 1e9, 2), "algorithmic_MB": round(by / 1e6, 1),
+            "achieved_TFLOPs": round(fl / sec / 1e12, 1), "frac_bf16_peak": round(fl / sec / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "bound": "mfma", "gemm_only_hipblaslt_us": tg,
+            "gemm_only_hipblaslt_TFLOPs": round(fl / (tg["median"] * 1e-6) / 1e12, 1)}
+
+
 def cpu_baseline(w, sched, budget_s: float = 12.0):
     """The fp64 oracle on the host cores over whole requests of the batch, until
     about `budget_s` seconds have been spent (at least one request)."""
@@ -439,6 +479,10 @@ def main() -> int:
     if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
         print("[bench] question-only diagnostic point", file=sys.stderr, flush=True)
         res["diagnostic_question_only"] = question_only_point(args.seed, stream)
+        torch.cuda.empty_cache()
+    if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
+        print("[bench] suffix QKV projection + rotary embedding + append", file=sys.stderr, flush=True)
+        res["qkv_projection"] = qkv_projection_point(w, args.seed, stream)
         torch.cuda.empty_cache()
     if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
         print("[bench] ordering strategies and tight-pool replay (host)", file=sys.stderr, flush=True)
