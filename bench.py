@@ -40,6 +40,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+SETTLE_S = 0.1              # untimed steps before the warm-up steps (clock settle)
 
 
 def attention_flops(prefix_len, suffix_len, hq, d) -> int:
@@ -370,27 +371,36 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     out = torch.empty_like(db.q)
     trace_mode = w.prefix_lens is None
-    # Two runners alternate, so a step never overwrites pinned host buffers
-    # whose upload an earlier step still has in flight.
+    # Two runners alternate. A step's schedule goes up on a copy stream while
+    # the previous step's kernels run: the upload of runner r waits until the
+    # kernels of r's last step are done with its device buffer (ev_done), the
+    # kernels wait for the upload (ev_up), and the host reuses r's pinned
+    # buffer only once that upload has completed.
+    copy_stream = torch.cuda.Stream(device=dev)
     runners = []
     for _ in range(2):
         rn = cw.BatchRunner([p.tokens(w.seed) for p in w.prompts], stride, hq, hkv, D, w.block_size, device=dev)
         rn.bind(db.q, db.k_new, db.v_new, db.k_cache, db.v_cache, out, w.scale, stream=stream)
-        rn.ev = None
+        rn.ev_up = None
+        rn.ev_done = None
         runners.append(rn)
     def step(i: int, ev=None):
         rn = runners[i % 2]
-        if rn.ev is not None:
-            rn.ev.synchronize()
+        if rn.ev_up is not None:
+            rn.ev_up.synchronize()
         pool = None
         if trace_mode:
             pool = snapshot.clone()
             rn.schedule(pool)
         else:
             rn.set_schedule(sched.block_table, sched.prefix_len, sched.cu_suffix)
-        rn.upload()
-        rn.ev = torch.cuda.Event()
-        rn.ev.record(stream)
+        with torch.cuda.stream(copy_stream):
+            if rn.ev_done is not None:
+                copy_stream.wait_event(rn.ev_done)
+            rn.upload()
+            rn.ev_up = torch.cuda.Event()
+            rn.ev_up.record(copy_stream)
+        stream.wait_event(rn.ev_up)
         if ev is None:
             rn.kv_append()
             rn.attention()
@@ -400,6 +410,8 @@ def main() -> int:
             ev[1].record(stream)
             rn.attention()
             ev[2].record(stream)
+        rn.ev_done = torch.cuda.Event()
+        rn.ev_done.record(stream)
         if pool is not None:
             rn.release(pool)
             pool.close()
@@ -408,7 +420,17 @@ def main() -> int:
     torch.cuda.synchronize()
     if runners[0].total_rows != total_s or not np.array_equal(runners[0].plen_host, P):
         raise RuntimeError("the scheduled batch differs from the prepared one")
-    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    # Settle: the card's clocks take tens of milliseconds of sustained load to
+    # reach their steady state (the attention kernel runs ~20 % slower in the
+    # first few milliseconds), so untimed steps run for at least SETTLE_S
+    # seconds before the warm-up steps, whatever --warmup is.
+    settle = 0
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < SETTLE_S:
+        step(settle)
+        settle += 1
+    torch.cuda.synchronize()
+    print(f"[bench] settle {settle} steps, warmup {args.warmup} steps", file=sys.stderr, flush=True)
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -448,6 +470,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_steps": settle,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True,
         "scaling": "weak",

@@ -57,18 +57,15 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // 0 .. of a single cache block. One workgroup per unit finds its (request,
 // unit) with a wave-wide prefix sum over the per-request unit counts, copies
 // the K rows ([slot][d] in the cache, contiguous 16-byte chunks) and writes V
-// transposed ([d][slot]) through LDS, 16-byte stores per 8-slot half row for
-// a full block and one element per slot for a partial one.
+// transposed ([d][slot]) by 8 x 8 register transposes: 16-byte stores per
+// 8-slot half row, one element per slot where a partial block ends.
 // ---------------------------------------------------------------------------
-constexpr int kAppendLds = 32768;   // bytes of V rows staged per pass
-
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(
     const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_cache,
     uint16_t* __restrict__ v_cache, const int32_t* __restrict__ bt, int bt_stride,
     const int32_t* __restrict__ cu, const int32_t* __restrict__ plen, int batch, int hkv, int D,
     int num_blocks) {
   __shared__ int s_unit[2];
-  __shared__ __attribute__((aligned(16))) uint16_t tile[kAppendLds / 2];
   const int tid = threadIdx.x;
   if (tid < 64) {
     const int b = blockIdx.x;
@@ -108,45 +105,59 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 
   const int nch = D / 8;   // 16-byte chunks per row and head
   const int64_t src0 = int64_t(cu0 + j0) * hkv * nch;
-  // K: source chunk c = (slot, head, chunk) -> cache [blk][head][slot][chunk]
+  // K: source chunk c = (slot, head, chunk) -> cache [blk][head][slot][chunk].
+  // A thread issues all loads of a batch before its stores.
   u32x4* kd = k_cache + int64_t(blk) * hkv * kBs * nch;
-  for (int c = tid; c < nv * hkv * nch; c += kThreads) {
-    const int ch = c & (nch - 1);
-    const int rest = c / nch;
-    const int h = rest % hkv;
-    const int slot = rest / hkv;
-    kd[(h * kBs + slot) * nch + ch] = k_new[src0 + c];
-  }
-  // V: stage [head][slot][d] in LDS, then write [blk][head][d][slot].
-  const int hc = max(1, kAppendLds / (kBs * D * 2));
-  uint16_t* vd = v_cache + int64_t(blk) * hkv * D * kBs;
-  for (int h0 = 0; h0 < hkv; h0 += hc) {
-    const int nh = min(hc, hkv - h0);
-    for (int c = tid; c < nv * nh * nch; c += kThreads) {
-      const int ch = c & (nch - 1);
-      const int rest = c / nch;
-      const int hl = rest % nh;
-      const int slot = rest / nh;
-      reinterpret_cast<u32x4*>(tile)[(hl * kBs + slot) * nch + ch] =
-          v_new[src0 + (int64_t(slot) * hkv + h0 + hl) * nch + ch];
-    }
-    __syncthreads();
-    for (int u = tid; u < nh * D * 2; u += kThreads) {
-      const int part = u & 1;
-      const int d = (u >> 1) & (D - 1);
-      const int hl = (u >> 1) / D;
-      const uint16_t* src = tile + (hl * kBs + 8 * part) * D + d;
-      uint16_t* dst = vd + (int64_t(h0 + hl) * D + d) * kBs + 8 * part;
-      if (nv == kBs) {
-        u32x4 w;
+  const int nk = nv * hkv * nch;
+  constexpr int kBatch = 8;
+  for (int c0 = tid; c0 < nk; c0 += kThreads * kBatch) {
+    u32x4 kr[kBatch];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = uint32_t(src[2 * j * D]) | (uint32_t(src[(2 * j + 1) * D]) << 16);
-        *reinterpret_cast<u32x4*>(dst) = w;
-      } else {
-        for (int j = 0; j < 8 && 8 * part + j < nv; ++j) dst[j] = src[j * D];
+    for (int i = 0; i < kBatch; ++i) kr[i] = k_new[src0 + min(c0 + i * kThreads, nk - 1)];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const int c = c0 + i * kThreads;
+      if (c < nk) {
+        const int ch = c & (nch - 1);
+        const int rest = c / nch;
+        kd[((rest % hkv) * kBs + rest / hkv) * nch + ch] = kr[i];
       }
     }
-    __syncthreads();
+  }
+  // V: the cache holds each block transposed, [blk][head][d][slot]. A task is
+  // (head, 8 values of d, 8 slots): it loads the 8 slots' 16-byte chunks,
+  // transposes the 8 x 8 block of bfloat16 in registers (v_perm) and stores 8
+  // rows of 8 slots. Slots past the unit's rows are neither read (the row index
+  // is clamped) nor written.
+  uint16_t* vd = v_cache + int64_t(blk) * hkv * D * kBs;
+  const int ntask = hkv * nch * 2;
+  for (int u = tid; u < ntask; u += kThreads) {
+    const int sh = u & 1;              // slots 8 sh .. 8 sh + 7
+    const int dc = (u >> 1) % nch;     // d = 8 dc .. 8 dc + 7
+    const int h = (u >> 1) / nch;
+    const int nvs = min(8, nv - 8 * sh);   // valid slots of this task
+    if (nvs <= 0) continue;
+    uint32_t rw[8][4];                 // rw[k][j]: slot 8 sh + k, d pair j
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int slot = min(8 * sh + k, nv - 1);
+      const u32x4 x = v_new[src0 + (int64_t(slot) * hkv + h) * nch + dc];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rw[k][j] = x[j];
+    }
+    uint16_t* dst = vd + (int64_t(h) * D + 8 * dc) * kBs + 8 * sh;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {      // output row d = 8 dc + e: 8 slots
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
+      uint32_t o[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = __builtin_amdgcn_perm(rw[2 * k + 1][e >> 1], rw[2 * k][e >> 1], sel);
+      if (nvs == 8) {
+        *reinterpret_cast<u32x4*>(dst + e * kBs) = u32x4{o[0], o[1], o[2], o[3]};
+      } else {
+        for (int k = 0; k < nvs; ++k) dst[e * kBs + k] = uint16_t(o[k >> 1] >> (16 * (k & 1)));
+      }
+    }
   }
 }
 
