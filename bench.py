@@ -100,6 +100,17 @@ def make_workload(name: str, seed: int):
     raise SystemExit(f"unknown workload {name}")
 
 
+def executed_mfma_flops(cu_suffix, prefix_len, hq: int, hkv: int, D: int) -> int:
+    """MFMA FLOPs the attention kernel executes: every tile of the plan runs
+    `cost` 64-key steps over all 256 packed rows (QK^T and PV), masked keys and
+    padding rows included. Divided by the algorithmic FLOPs this is the
+    masked-tile waste factor."""
+    from paper_2606_19667_amd import cw
+    plan, n = cw.suffix_prefill_plan(cu_suffix, prefix_len, hq, hkv, D)
+    steps = int(plan.reshape(-1, 4)[:n, 3][plan.reshape(-1, 4)[:n, 0] >= 0].astype(np.int64).sum())
+    return steps * 256 * 64 * D * 4
+
+
 def percentiles_us(times_ms):
     t = np.asarray(times_ms, dtype=np.float64) * 1e3
     return {"median": round(float(np.median(t)), 2), "p10": round(float(np.percentile(t, 10)), 2),
@@ -223,6 +234,31 @@ def question_only_point(seed: int, stream):
         del ws
     res["split_auto"] = cw.split_count(db.meta)
     return res
+
+
+def mfma_peak_point(seed: int, stream, workgroups: int = 1024, iters: int = 2000) -> dict:
+    """The bf16 MFMA rate this card sustains (cw_probe_mfma_bf16: 8 independent
+    32x32x16 accumulators per wave, two waves per SIMD, no memory traffic), on
+    normal random bf16 fragments like the workload's Q/K/V and on all-zero
+    fragments. The power limit lowers the clock more for random operand bits,
+    so the first is the ceiling that applies to the attention kernel; the
+    roofline above stays priced against the data-sheet 2.5 PFLOP/s."""
+    import torch
+    from paper_2606_19667_amd import cw, inputs
+    n = 4096 * 512
+    sink = torch.empty(workgroups * 512, dtype=torch.float32, device="cuda")
+    fl = cw.probe_mfma_bf16_flops(iters, workgroups)
+    out = {"kernel": "mfma_probe_kernel (v_mfma_f32_32x32x16_bf16, 8 waves per CU)", "GFLOP_per_call": round(fl / 1e9, 2)}
+    for name, ops in (("normal_bf16", inputs.normal_bf16((seed, 301), (n,), "cuda")),
+                      ("zero", torch.zeros(n, dtype=torch.bfloat16, device="cuda"))):
+        fn = lambda: cw.probe_mfma_bf16(ops, sink, iters, workgroups, stream=stream)
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < SETTLE_S:
+            fn()
+            torch.cuda.synchronize()
+        t = percentiles_us(timed_calls(fn, stream, 10))
+        out[name] = {"us": t, "TFLOPs": round(fl / (t["median"] * 1e-6) / 1e12, 1)}
+    return out
 
 
 def qkv_projection_point(w, seed: int, stream, hidden: int = 4096, rope_base: float = 500000.0):
@@ -463,6 +499,7 @@ def main() -> int:
     host = host_timing(w, snapshot, stride) if trace_mode else None
 
     achieved = flops / (attn_ms * 1e-3) / 1e12
+    mfma_flops = executed_mfma_flops(sched.cu_suffix, P, hq, hkv, D)
     res = {
         "metric": "suffix-prefill attention TFLOP/s (whole step: schedule + kv_append + attention)",
         "value": round(flops / (ms_per_step * 1e-3) / 1e12, 3),
@@ -487,6 +524,8 @@ def main() -> int:
         "kv_append_us": round(app_ms * 1e3, 2),
         "kv_append_GBps": round(append_bytes(S, hkv, D) / (app_ms * 1e-3) / 1e9, 1),
         "attention_GFLOP": round(flops / 1e9, 3),
+        "attention_mfma_GFLOP": round(mfma_flops / 1e9, 3),
+        "mfma_waste_factor": round(mfma_flops / flops, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": counted_traffic(args.workload),
@@ -507,6 +546,11 @@ def main() -> int:
         print("[bench] suffix QKV projection + rotary embedding + append", file=sys.stderr, flush=True)
         res["qkv_projection"] = qkv_projection_point(w, args.seed, stream)
         torch.cuda.empty_cache()
+    if not args.no_diagnostic:
+        print("[bench] sustained bf16 MFMA rate (measurement aid)", file=sys.stderr, flush=True)
+        mp = mfma_peak_point(args.seed, stream)
+        mp["attention_frac_of_normal_bf16"] = round(achieved / mp["normal_bf16"]["TFLOPs"], 4)
+        res["mfma_peak_measured"] = mp
     if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
         print("[bench] ordering strategies and tight-pool replay (host)", file=sys.stderr, flush=True)
         res["ordering"] = ordering_point(args.seed)

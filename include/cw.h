@@ -393,6 +393,29 @@ cw_status cw_qkv_rope_append(const void* x, const void* w, const void* bias, con
                              int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t num_blocks,
                              void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Measurement aid (not a step of the path). A roofline of the attention kernel
+ * prices it against the data-sheet bf16 peak; the rate this card sustains
+ * depends on the operand values through its power limit, so the bench reports
+ * the measured rate beside the data-sheet one.
+ *
+ * cw_probe_mfma_bf16 launches `workgroups` workgroups of 8 wavefronts; each
+ * wavefront runs `iters` rounds of 8 independent v_mfma_f32_32x32x16_bf16
+ * instructions (32x32 accumulators, 16-deep bf16 products) on fragments read
+ * once from `operands`.
+ *   operands       device, bf16 values, operand_bytes bytes: fragments of
+ *                  1024 bytes (16 per lane), used cyclically; read only
+ *   operand_bytes  a multiple of 1024, >= 6144
+ *   sink           device float[workgroups * 512]; one value per thread is
+ *                  written (the accumulator sum), only so the work is kept
+ *   iters >= 1; 1 <= workgroups <= 2^20. Asynchronous on `stream`.
+ * CW_EINVAL: NULL pointer or a size out of range. CW_EHIP: launch failure.
+ * cw_probe_mfma_bf16_flops returns the FLOPs of one such call (2 x 32 x 32 x 16
+ * per instruction), or -1 for iters < 1 or workgroups < 1. */
+int64_t cw_probe_mfma_bf16_flops(int32_t iters, int32_t workgroups);
+cw_status cw_probe_mfma_bf16(const void* operands, int64_t operand_bytes, float* sink, int32_t iters,
+                             int32_t workgroups, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,7 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["cw_host.cpp", "cw_tree.cpp", "cw_proj.cpp"]
-HIP_SOURCES = ["cw_kernels.hip", "cw_qkv.hip"]
+HIP_SOURCES = ["cw_kernels.hip", "cw_qkv.hip", "cw_probe.hip"]
 
 HIP_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

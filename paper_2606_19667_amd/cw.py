@@ -83,6 +83,8 @@ def _load() -> ctypes.CDLL:
         "cw_rope_table": (_i32, [_i32, _i32, ctypes.c_double, ctypes.POINTER(ctypes.c_float)]),
         "cw_qkv_rope_append": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
                                       _pi32, _pi32, _i32, _i32, _i32, _i32, _i32, _i32, _vp]),
+        "cw_probe_mfma_bf16_flops": (_i64, [_i32, _i32]),
+        "cw_probe_mfma_bf16": (_i32, [_vp, _i64, _vp, _i32, _i32, _vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -100,7 +102,8 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
             "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge",
             "cw_tree_create", "cw_tree_destroy", "cw_tree_num_nodes", "cw_tree_insert",
-            "cw_tree_mark_stale", "cw_tree_order", "cw_rope_table", "cw_qkv_rope_append")
+            "cw_tree_mark_stale", "cw_tree_order", "cw_rope_table", "cw_qkv_rope_append",
+            "cw_probe_mfma_bf16_flops", "cw_probe_mfma_bf16")
 
 
 def lib() -> ctypes.CDLL:
@@ -637,3 +640,24 @@ class BatchRunner:
             raise ValueError("bound tensors do not match the scheduled suffix rows")
         self._attn_args[17] = self.num_tiles
         _check(_lib.cw_suffix_prefill_attn(*self._attn_args))
+
+
+# ---------------------------------------------------------------- measurement aid
+def probe_mfma_bf16_flops(iters: int, workgroups: int) -> int:
+    """FLOPs of one cw_probe_mfma_bf16 call."""
+    n = int(_lib.cw_probe_mfma_bf16_flops(int(iters), int(workgroups)))
+    if n < 0:
+        raise ValueError("iters and workgroups must be >= 1")
+    return n
+
+
+def probe_mfma_bf16(operands: torch.Tensor, sink: torch.Tensor, iters: int, workgroups: int, stream=None) -> None:
+    """cw_probe_mfma_bf16: back-to-back bf16 MFMA work on fragments of `operands`
+    (bf16, a multiple of 512 values); `sink` (float32) receives one value per
+    thread and must hold workgroups * 512. Not a step of the path: it measures
+    the matrix rate the card sustains on data of a given distribution."""
+    if sink.numel() < int(workgroups) * 512:
+        raise ValueError(f"sink must hold {int(workgroups) * 512} floats")
+    _check(_lib.cw_probe_mfma_bf16(_dev(operands, torch.bfloat16, "operands"), operands.numel() * 2,
+                                   _dev(sink, torch.float32, "sink"), int(iters), int(workgroups),
+                                   _stream(stream)))

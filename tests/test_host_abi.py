@@ -399,3 +399,20 @@ def test_host_calls_reject_bad_arguments():
         p.commit([5, 6], [a[0], a[0]])
     with pytest.raises(cw.CwError):
         cw.suffix_prefill_plan([0, 10], [0], 32, 8, 96)
+
+
+def test_probe_mfma_flops_and_argument_errors():
+    # FLOPs of one call: 8 waves x iters x 8 instructions x 2*32*32*16 per workgroup
+    assert cw.probe_mfma_bf16_flops(1, 1) == 8 * 8 * 32768
+    assert cw.probe_mfma_bf16_flops(2000, 1024) == 1024 * 8 * 2000 * 8 * 32768
+    with pytest.raises(ValueError):
+        cw.probe_mfma_bf16_flops(0, 1)
+    lib = cw.lib()
+    dummy = ctypes.c_void_p(16)   # never dereferenced: every case fails its checks first
+    assert lib.cw_probe_mfma_bf16(None, 8192, dummy, 1, 1, None) == cw.CW_EINVAL
+    assert lib.cw_probe_mfma_bf16(dummy, 8192, None, 1, 1, None) == cw.CW_EINVAL
+    assert lib.cw_probe_mfma_bf16(dummy, 5120, dummy, 1, 1, None) == cw.CW_EINVAL    # < 6 fragments
+    assert lib.cw_probe_mfma_bf16(dummy, 8193, dummy, 1, 1, None) == cw.CW_EINVAL    # not whole fragments
+    assert lib.cw_probe_mfma_bf16(dummy, 8192, dummy, 0, 1, None) == cw.CW_EINVAL
+    assert lib.cw_probe_mfma_bf16(dummy, 8192, dummy, 1, 0, None) == cw.CW_EINVAL
+    assert "probe_mfma_bf16" in cw.last_error()
