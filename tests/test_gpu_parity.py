@@ -160,12 +160,14 @@ def test_attention_small_trace_batch_full():
     _cleanup()
 
 
-def test_attention_trace_batch16_sampled():
-    w = W.llama8b_trace_batch(seed=0)
-    _say(f"attention {w.name}")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_attention_trace_batch16_sampled(seed):
+    """The measured 16-request batch at full size; seed 0 is the bench batch."""
+    w = W.llama8b_trace_batch(seed=seed)
+    _say(f"attention {w.name} seed={seed}")
     db = B.materialize(w)
     _say(f"  prefix_len={db.sched.prefix_len.tolist()}")
-    _compare_sampled(db, _run(db), range(w.batch))
+    _compare_sampled(db, _run(db), range(w.batch), seed=seed)
     _cleanup()
 
 
