@@ -331,6 +331,25 @@ def _stream(stream) -> int:
     return int(stream.cuda_stream)
 
 
+# Debug mode: every device call first checks that the device copies of the
+# batch description (block table, offsets, prefix lengths, plan) equal the host
+# copies that validated it. The check synchronises the device; off by default.
+DEBUG_CHECK_COPIES = os.environ.get("CW_DEBUG_CHECK_COPIES", "") not in ("", "0")
+
+
+def _check_copies(pairs) -> None:
+    """Raises ValueError naming the first (name, device tensor, host array)
+    whose device copy is missing or differs from the host copy."""
+    if torch.cuda.is_available():
+        torch.cuda.synchronize()
+    for name, dev, host in pairs:
+        if dev is None:
+            raise ValueError(f"{name}: no device copy")
+        got = dev.detach().to("cpu").numpy()
+        if got.shape != host.shape or not np.array_equal(got, host):
+            raise ValueError(f"{name}: the device copy differs from the host copy")
+
+
 class BatchMeta:
     """Host and device copies of a ragged batch's description.
 
@@ -371,6 +390,14 @@ class BatchMeta:
     def _hp(self, a):
         return _ptr(a, ctypes.c_int32)
 
+    def check_device_copies(self) -> None:
+        """The caller guarantees that the device copies equal the host ones
+        (the library validates and plans with the host copies, the kernels
+        read the device copies); this checks it, synchronising the device."""
+        plan = self.plan_host if self.plan_host.size else np.zeros(4, np.int32)
+        _check_copies((("block_table", self.bt, self.bt_host), ("cu_suffix", self.cu, self.cu_host),
+                       ("prefix_len", self.plen, self.plen_host), ("plan", self.plan, plan)))
+
 
 def _cache_shapes_ok(k_cache: torch.Tensor, v_cache: torch.Tensor, hkv: int, D: int) -> bool:
     """K blocks are [slot][d], V blocks [d][slot]; both caches hold the same blocks."""
@@ -381,6 +408,8 @@ def _cache_shapes_ok(k_cache: torch.Tensor, v_cache: torch.Tensor, hkv: int, D: 
 def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor,
               v_cache: torch.Tensor, stream=None) -> None:
     """cw_kv_append: write the suffix K/V rows into their cache blocks."""
+    if DEBUG_CHECK_COPIES:
+        meta.check_device_copies()
     hkv, D = meta.num_kv_heads, meta.head_dim
     for name, t in (("k_new", k_new), ("v_new", v_new)):
         if tuple(t.shape) != (meta.total_rows, hkv, D):
@@ -402,6 +431,8 @@ def qkv_rope_append(meta: BatchMeta, x: torch.Tensor, w: torch.Tensor, rope: tor
     [(Hq + 2 Hkv) D, hidden] (+ bias), rotate q and k at their positions with
     the table rope [n, D/2, 2] (cw.rope_table on the device), write k and v into
     the cache blocks and return q_out [total_s, Hq, D] bf16."""
+    if DEBUG_CHECK_COPIES:
+        meta.check_device_copies()
     hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
     if x.dim() != 2 or x.shape[0] != meta.total_rows:
         raise ValueError(f"x must be [{meta.total_rows}, hidden], got {tuple(x.shape)}")
@@ -434,6 +465,8 @@ def qkv_rope_append(meta: BatchMeta, x: torch.Tensor, w: torch.Tensor, rope: tor
 def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                         softmax_scale: float, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """cw_suffix_prefill_attn: attention of the suffix rows; returns out [total_s, Hq, D] bf16."""
+    if DEBUG_CHECK_COPIES:
+        meta.check_device_copies()
     hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
     if tuple(q.shape) != (meta.total_rows, hq, D):
         raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
@@ -472,6 +505,8 @@ def suffix_prefill_attn_split(meta: BatchMeta, q: torch.Tensor, k_cache: torch.T
                               stream=None) -> torch.Tensor:
     """cw_suffix_prefill_attn_split: the split-KV path; returns out [total_s, Hq, D] bf16.
     `workspace` (uint8, device) is allocated when not given."""
+    if DEBUG_CHECK_COPIES:
+        meta.check_device_copies()
     hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
     if num_splits is None:
         num_splits = split_count(meta)
@@ -630,14 +665,24 @@ class BatchRunner:
                            out.data_ptr(), s]
         self._rows = (q.shape[0], k_new.shape[0], v_new.shape[0], out.shape[0])
 
+    def check_device_copies(self) -> None:
+        """Checks that the uploaded schedule equals the host one (synchronises)."""
+        n = 4 * max(self.num_tiles, 1)
+        _check_copies((("block_table", self.bt, self.bt_host), ("cu_suffix", self.cu, self.cu_host),
+                       ("prefix_len", self.plen, self.plen_host), ("plan", self.plan[:n], self.plan_host[:n])))
+
     def kv_append(self) -> None:
         if any(n != self.total_rows for n in self._rows):
             raise ValueError("bound tensors do not match the scheduled suffix rows")
+        if DEBUG_CHECK_COPIES:
+            self.check_device_copies()
         _check(_lib.cw_kv_append(*self._append_args))
 
     def attention(self) -> None:
         if any(n != self.total_rows for n in self._rows):
             raise ValueError("bound tensors do not match the scheduled suffix rows")
+        if DEBUG_CHECK_COPIES:
+            self.check_device_copies()
         self._attn_args[17] = self.num_tiles
         _check(_lib.cw_suffix_prefill_attn(*self._attn_args))
 

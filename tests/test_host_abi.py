@@ -416,3 +416,23 @@ def test_probe_mfma_flops_and_argument_errors():
     assert lib.cw_probe_mfma_bf16(dummy, 8192, dummy, 0, 1, None) == cw.CW_EINVAL
     assert lib.cw_probe_mfma_bf16(dummy, 8192, dummy, 1, 0, None) == cw.CW_EINVAL
     assert "probe_mfma_bf16" in cw.last_error()
+
+
+def test_debug_check_of_device_copies():
+    # CPU tensors stand in for the device copies: the check compares values only
+    bt = np.array([[3, 1, 0, -1], [2, 4, -1, -1]], dtype=np.int32)
+    meta = cw.BatchMeta(bt, [0, 20, 30], [32, 16], 4, 1, 64, device=None)
+    import torch
+    meta.bt, meta.cu, meta.plen = (torch.from_numpy(a.copy()) for a in (meta.bt_host, meta.cu_host, meta.plen_host))
+    meta.plan = torch.from_numpy(meta.plan_host.copy())
+    meta.check_device_copies()
+    meta.cu[2] = 31
+    with pytest.raises(ValueError, match="cu_suffix"):
+        meta.check_device_copies()
+    meta.cu[2] = 30
+    meta.plan[3] += 1
+    with pytest.raises(ValueError, match="plan"):
+        meta.check_device_copies()
+    meta.plan = None
+    with pytest.raises(ValueError, match="no device copy"):
+        meta.check_device_copies()
