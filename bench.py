@@ -301,6 +301,18 @@ def qkv_projection_point(w, seed: int, stream, hidden: int = 4096, rope_base: fl
             "gemm_only_hipblaslt_TFLOPs": round(fl / (tg["median"] * 1e-6) / 1e12, 1)}
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (first processor entry of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, sched, budget_s: float = 12.0):
     """The fp64 oracle on the host cores over whole requests of the batch, until
     about `budget_s` seconds have been spent (at least one request)."""
@@ -329,6 +341,7 @@ def cpu_baseline(w, sched, budget_s: float = 12.0):
                 break
     return {"value": round(flops / elapsed / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle", "sample": f"{n} of {w.batch} requests (all heads and rows), fp64 NumPy",
+            "cpu_model": cpu_model(),
             "seconds": round(elapsed, 3), "suffix_tokens_per_s": round(tokens / elapsed, 1)}
 
 
