@@ -13,12 +13,16 @@
 //   v -> V cache [blk][g][d][slot] (each block stored transposed)
 //
 // Design (one workgroup = 8 wavefronts = one 256-feature x 256-token tile):
-//  * The product is formed as C^T = W x^T with v_mfma_f32_32x32x16_bf16:
-//    A = 32 rows of W, B = 32 token rows of x. In the 32x32 accumulator a
-//    lane then holds one token and 16 features, so everything the epilogue
-//    needs per element (position, block, slot) is per lane.
+//  * The product is formed as C^T = W x^T with v_mfma_f32_16x16x32_bf16:
+//    A = 16 rows of W, B = 16 token rows of x, 32 hidden per instruction (one
+//    pipeline step). In the 16x16 accumulator a lane holds one token and 4
+//    consecutive features, so everything the epilogue needs per element
+//    (position, block, slot) is per lane. This shape sustains a higher rate
+//    than 32x32x16 on random data (the card's power limit lowers the clock
+//    less for it).
 //  * Wave (wf, wt) owns features {j0 .. j0 + 31} and {j0 + D/2 .. + 31} of one
-//    head and 128 tokens. The two feature blocks are exactly the rotary pairs
+//    head (four 16-row blocks) and 128 tokens (eight 16-token blocks). The
+//    blocks j0 + 16 p and j0 + D/2 + 16 p are exactly rotary pairs
 //    (j, j + D/2), which therefore sit in the same lane and register of two
 //    accumulators: the rotation needs no data exchange.
 //  * Hidden is walked in steps of 32. Four LDS stages of 32 KB (W rows then x
@@ -136,21 +140,24 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
   // ---- operand rows of this wave
   constexpr int kWavesPerHead = D / 64;
   const int wf = wave & 3, wt = wave >> 2;
-  const int head_l = wf / kWavesPerHead;                 // head inside the tile
-  const int j0 = (wf % kWavesPerHead) * 32;              // first rotary index of the wave
-  const int arow0 = head_l * D + j0;                     // tile rows of the two W blocks
-  const int arow1 = arow0 + D / 2;
-  const int brow = wt * 128;                             // first tile token of the wave
-  // in-stage byte offset of slice kk for a block starting at a multiple of 32 rows
-  int sw[2];
+  const int head_l = wf / kWavesPerHead;
+  const int j0 = (wf % kWavesPerHead) * 32;
+  const int arow0 = head_l * D + j0;
+  const int brow = wt * 128;
+  const int l16 = lane & 15;
+  const int g4 = lane >> 4;
+  // 16-row block starting at a multiple of 16 rows: lane reads row l16, chunk g4 (swizzled)
+  const int so = l16 * kRow + ((g4 ^ row_swz(l16)) << 4);
+  // feature blocks: fa = 0, 1 -> j0 + 16 fa; fa = 2, 3 -> j0 + D/2 + 16 (fa - 2)
+  int arow[4];
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) sw[kk] = l32 * kRow + (((2 * kk + half) ^ row_swz(l32)) << 4);
+  for (int fa = 0; fa < 4; ++fa) arow[fa] = arow0 + (fa >> 1) * (D / 2) + (fa & 1) * 16;
 
-  f32x16 acc0[4], acc1[4];
+  f32x4 acc[4][8];
 #pragma unroll
-  for (int tb = 0; tb < 4; ++tb)
+  for (int fa = 0; fa < 4; ++fa)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc0[tb][e] = acc1[tb][e] = 0.f;
+    for (int tb = 0; tb < 8; ++tb) acc[fa][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = hidden / kStep;
 #pragma unroll
@@ -158,7 +165,6 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
     if (s < nk) issue(s, s);
 
   for (int k = 0; k < nk; ++k) {
-    // this wave's copies of step k have landed (later steps may be in flight)
     const int later = min(nk - 1 - k, kAhead - 1);
     if (later >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * kCopies));
     else if (later == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kCopies));
@@ -166,56 +172,44 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    // stage (k + 3) % 4 was last read in step k - 1, which every wave has left
     if (k + kAhead < nk) issue(k + kAhead, (k + kAhead) % kStages);
 
     const uint8_t* st = lds + (k % kStages) * kStage;
+    bf16x8 a[4], bx[8];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const bf16x8 a0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + arow0 * kRow + sw[kk]));
-      const bf16x8 a1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + arow1 * kRow + sw[kk]));
-      bf16x8 bx[4];
+    for (int fa = 0; fa < 4; ++fa)
+      a[fa] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + arow[fa] * kRow + so));
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-        bx[tb] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(st + kPart + (brow + 32 * tb) * kRow + sw[kk]));
+    for (int tb = 0; tb < 8; ++tb)
+      bx[tb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + kPart + (brow + 16 * tb) * kRow + so));
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        acc0[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bx[tb], acc0[tb], 0, 0, 0);
-        acc1[tb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bx[tb], acc1[tb], 0, 0, 0);
-      }
-    }
+    for (int tb = 0; tb < 8; ++tb)
+#pragma unroll
+      for (int fa = 0; fa < 4; ++fa)
+        acc[fa][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[fa], bx[tb], acc[fa][tb], 0, 0, 0);
   }
 
   // ---- epilogue: bias, rotation, bf16 rounding, stores
-  const int hf = (f0 + head_l * D) / D;   // global head index of the wave's features
-  if (hf >= hq + 2 * hkv) return;         // past the last head (partial feature tile)
-  const int kind = hf < hq ? 0 : (hf < hq + hkv ? 1 : 2);   // q, k or v
+  const int hf = (f0 + head_l * D) / D;
+  if (hf >= hq + 2 * hkv) return;
+  const int kind = hf < hq ? 0 : (hf < hq + hkv ? 1 : 2);
   const int g = kind == 1 ? hf - hq : hf - hq - hkv;
-  // rotary index / head-dim offset of register e of block 0: j0 + dq(e)
-  // with dq(e) = 8 (e / 4) + 4 half + e % 4; block 1 is + D / 2.
-  float bb0[16], bb1[16];
-  if (bias) {
-    const uint16_t* bp = bias + int64_t(hf) * D + j0 + 4 * half;
+  // element e of acc[fa][tb]: feature j0 + 16 (fa & 1) + 4 g4 + e (+ D/2 for fa >= 2), token brow + 16 tb + l16
+  float bb[4][4];
 #pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      const u32x2 v0 = *reinterpret_cast<const u32x2*>(bp + 8 * q4);
-      const u32x2 v1 = *reinterpret_cast<const u32x2*>(bp + 8 * q4 + D / 2);
-      bb0[4 * q4 + 0] = bf16_lo(v0[0]); bb0[4 * q4 + 1] = bf16_hi(v0[0]);
-      bb0[4 * q4 + 2] = bf16_lo(v0[1]); bb0[4 * q4 + 3] = bf16_hi(v0[1]);
-      bb1[4 * q4 + 0] = bf16_lo(v1[0]); bb1[4 * q4 + 1] = bf16_hi(v1[0]);
-      bb1[4 * q4 + 2] = bf16_lo(v1[1]); bb1[4 * q4 + 3] = bf16_hi(v1[1]);
+  for (int fa = 0; fa < 4; ++fa) {
+    if (bias) {
+      const u32x2 v = *reinterpret_cast<const u32x2*>(bias + int64_t(hf) * D + j0 + (fa >> 1) * (D / 2) + (fa & 1) * 16 + 4 * g4);
+      bb[fa][0] = bf16_lo(v[0]); bb[fa][1] = bf16_hi(v[0]); bb[fa][2] = bf16_lo(v[1]); bb[fa][3] = bf16_hi(v[1]);
+    } else {
+      bb[fa][0] = bb[fa][1] = bb[fa][2] = bb[fa][3] = 0.f;
     }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 16; ++e) bb0[e] = bb1[e] = 0.f;
   }
 
 #pragma unroll
-  for (int tb = 0; tb < 4; ++tb) {
-    const int t = t0 + brow + 32 * tb + l32;
+  for (int tb = 0; tb < 8; ++tb) {
+    const int t = t0 + brow + 16 * tb + l16;
     if (t >= T) continue;
-    // request of token t: the largest r with cu[r] <= t
     int lo = 0, hi = batch - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -223,61 +217,50 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
       else hi = mid - 1;
     }
     const int pos = plen[lo] + (t - cu[lo]);
-    float o0[16], o1[16];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      o0[e] = acc0[tb][e] + bb0[e];
-      o1[e] = acc1[tb][e] + bb1[e];
+    int blk = 0, slot = 0;
+    if (kind != 0) {
+      blk = bt[int64_t(lo) * bt_stride + pos / kBs];
+      if (blk < 0 || blk >= num_blocks) continue;
+      slot = pos % kBs;
     }
-    if (kind != 2) {
-      const float* cs = rope + (int64_t(pos) * (D / 2) + j0 + 4 * half) * 2;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const f32x4 c01 = *reinterpret_cast<const f32x4*>(cs + 16 * q4);
-        const f32x4 c23 = *reinterpret_cast<const f32x4*>(cs + 16 * q4 + 4);
+    for (int p = 0; p < 2; ++p) {
+      const int j = j0 + 16 * p + 4 * g4;   // rotary index of element 0
+      float o0[4], o1[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o0[e] = acc[p][tb][e] + bb[p][e];
+        o1[e] = acc[p + 2][tb][e] + bb[p + 2][e];
+      }
+      if (kind != 2) {
+        const float* cs = rope + (int64_t(pos) * (D / 2) + j) * 2;
+        const f32x4 c01 = *reinterpret_cast<const f32x4*>(cs);
+        const f32x4 c23 = *reinterpret_cast<const f32x4*>(cs + 4);
         const float c[4] = {c01[0], c01[2], c23[0], c23[2]};
-        const float s[4] = {c01[1], c01[3], c23[1], c23[3]};
+        const float sn[4] = {c01[1], c01[3], c23[1], c23[3]};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float a = o0[4 * q4 + i], bv = o1[4 * q4 + i];
-          o0[4 * q4 + i] = a * c[i] - bv * s[i];
-          o1[4 * q4 + i] = bv * c[i] + a * s[i];
+        for (int e = 0; e < 4; ++e) {
+          const float av = o0[e], bv = o1[e];
+          o0[e] = av * c[e] - bv * sn[e];
+          o1[e] = bv * c[e] + av * sn[e];
         }
       }
-    }
-    if (kind == 0) {
-      uint16_t* qp = q_out + (int64_t(t) * hq + hf) * D + j0 + 4 * half;
+      if (kind == 0) {
+        uint16_t* qp = q_out + (int64_t(t) * hq + hf) * D + j;
+        *reinterpret_cast<u32x2*>(qp) = u32x2{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3])};
+        *reinterpret_cast<u32x2*>(qp + D / 2) = u32x2{pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
+      } else if (kind == 1) {
+        uint16_t* kp = k_cache + ((int64_t(blk) * hkv + g) * kBs + slot) * D + j;
+        *reinterpret_cast<u32x2*>(kp) = u32x2{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3])};
+        *reinterpret_cast<u32x2*>(kp + D / 2) = u32x2{pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
+      } else {
+        uint16_t* vp = v_cache + ((int64_t(blk) * hkv + g) * D + j) * kBs + slot;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        *reinterpret_cast<u32x2*>(qp + 8 * q4) =
-            u32x2{pack_bf16x2(o0[4 * q4], o0[4 * q4 + 1]), pack_bf16x2(o0[4 * q4 + 2], o0[4 * q4 + 3])};
-        *reinterpret_cast<u32x2*>(qp + 8 * q4 + D / 2) =
-            u32x2{pack_bf16x2(o1[4 * q4], o1[4 * q4 + 1]), pack_bf16x2(o1[4 * q4 + 2], o1[4 * q4 + 3])};
-      }
-      continue;
-    }
-    const int blk = bt[int64_t(lo) * bt_stride + pos / kBs];
-    if (blk < 0 || blk >= num_blocks) continue;
-    const int slot = pos % kBs;
-    if (kind == 1) {
-      uint16_t* kp = k_cache + ((int64_t(blk) * hkv + g) * kBs + slot) * D + j0 + 4 * half;
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        *reinterpret_cast<u32x2*>(kp + 8 * q4) =
-            u32x2{pack_bf16x2(o0[4 * q4], o0[4 * q4 + 1]), pack_bf16x2(o0[4 * q4 + 2], o0[4 * q4 + 3])};
-        *reinterpret_cast<u32x2*>(kp + 8 * q4 + D / 2) =
-            u32x2{pack_bf16x2(o1[4 * q4], o1[4 * q4 + 1]), pack_bf16x2(o1[4 * q4 + 2], o1[4 * q4 + 3])};
-      }
-    } else {
-      uint16_t* vp = v_cache + ((int64_t(blk) * hkv + g) * D + j0 + 4 * half) * kBs + slot;
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int d = 8 * q4 + i;
-          vp[d * kBs] = uint16_t(pack_bf16x2(o0[4 * q4 + i], 0.f));
-          vp[(d + D / 2) * kBs] = uint16_t(pack_bf16x2(o1[4 * q4 + i], 0.f));
+        for (int e = 0; e < 4; ++e) {
+          vp[e * kBs] = uint16_t(pack_bf16x2(o0[e], 0.f));
+          vp[(e + D / 2) * kBs] = uint16_t(pack_bf16x2(o1[e], 0.f));
         }
+      }
     }
   }
 }
