@@ -181,9 +181,10 @@ typedef struct cw_tree cw_tree;
 #define CW_ORDER_RECENCY 2    /* documents served within the window first, latest
                                  first (ties in retrieval rank), then the rest in
                                  retrieval rank */
-#define CW_ORDER_GREEDY 3     /* Algorithm 1: walk from the root, placing the first
-                                 remaining document (in retrieval rank) whose child
-                                 is cached; then the rest in retrieval rank */
+#define CW_ORDER_GREEDY 3     /* Algorithm 1: from the root, repeatedly place the
+                                 unplaced document of lowest retrieval rank whose
+                                 child node is cached; when none is, the rest
+                                 follow in retrieval rank */
 #define CW_ORDER_EXHAUSTIVE 4 /* Eq. 1: an order of maximal l(O, T); among equally
                                  deep reused runs the one first in lexicographic
                                  order of retrieval ranks; then the rest in
@@ -209,8 +210,13 @@ cw_status cw_tree_mark_stale(cw_tree* tree, const int64_t* order, int32_t k, int
 
 /* Orders the retrieved set `docs` [k] with `strategy` (CW_ORDER_*), writing the
  * permutation to out_order [k]. *out_depth = l(out_order, T). *out_probes =
- * child lookups made (Algorithm 1: at most k (k + 1) / 2). out_depth and
- * out_probes may be NULL. The tree is not modified.
+ * child lookups: for the walk of the retrieval, sorted and recency orders, one
+ * per node visited plus the failing one; for the greedy order, the lookups a
+ * scan of the unplaced documents in retrieval rank makes to find each choice
+ * (at a level that places rank j, one per unplaced rank <= j; at the level
+ * that finds none, one per unplaced document; at most k (k + 1) / 2); for the
+ * exhaustive order, the lookups of its search. out_depth and out_probes may be
+ * NULL. The tree is not modified.
  * CW_EINVAL: tree NULL, k outside [0, 4096], NULL arrays with k > 0, repeated
  * IDs, unknown strategy. */
 cw_status cw_tree_order(const cw_tree* tree, int32_t strategy, const int64_t* docs, int32_t k,

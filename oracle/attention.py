@@ -117,12 +117,6 @@ def suffix_prefill_attention_loops(q, k, v, prefix_len: int, scale: float) -> np
     return out
 
 
-def batch_suffix_prefill_attention(qs, ks, vs, prefix_lens, scale: float) -> list:
-    """Per-request outputs for a ragged batch (lists of per-request arrays)."""
-    return [suffix_prefill_attention(q, k, v, p, scale)
-            for q, k, v, p in zip(qs, ks, vs, prefix_lens)]
-
-
 def suffix_prefill_rows(q, k, v, prefix_len: int, scale: float, rows,
                         row_chunk: int = 256) -> np.ndarray:
     """Output of selected suffix rows only: [len(rows), Hq, D] float64.

@@ -112,26 +112,29 @@ def walk_depth(order, is_cached) -> int:
 
 
 def greedy_order(docs, is_cached):
-    """Algorithm 1. From the root, scan the remaining documents in retrieval
-    rank; the first whose child node exists and is cached is placed next and
-    the walk moves to that child. When none is, the remaining documents follow
-    in retrieval rank. Returns (order, depth, probes); probes counts child
-    lookups, one per scanned document."""
-    order, rest, path, probes = [], list(docs), (), 0
-    while rest:
-        nxt = None
-        for d in rest:
-            probes += 1
-            if is_cached(path + (d,)):
-                nxt = d
-                break
-        if nxt is None:
-            order.extend(rest)
+    """The greedy order of Sec. 3.3 (Algorithm 1), stated by what it selects:
+    the reused run r_1, r_2, ... is built one level at a time, r_j being the
+    document of lowest retrieval rank among those not yet placed whose node
+    below (r_1 .. r_{j-1}) is cached; the run ends at the first level with no
+    such document, and the unplaced documents follow in retrieval rank.
+
+    Returns (order, depth, probes). probes is the number of child lookups a
+    scan in retrieval rank makes to find those choices: at a level that places
+    document d, one per unplaced document of rank up to d's; at the level that
+    finds nothing (when documents remain), one per unplaced document."""
+    rank = {d: i for i, d in enumerate(docs)}
+    run = ()
+    probes = 0
+    while True:
+        unplaced = [d for d in docs if d not in run]
+        candidates = [d for d in unplaced if is_cached(run + (d,))]
+        if not candidates:
+            probes += len(unplaced)
             break
-        order.append(nxt)
-        rest.remove(nxt)
-        path = path + (nxt,)
-    return order, len(path), probes
+        pick = min(candidates, key=rank.__getitem__)
+        probes += sum(1 for d in unplaced if rank[d] <= rank[pick])
+        run = run + (pick,)
+    return list(run) + [d for d in docs if d not in run], len(run), probes
 
 
 def exhaustive_order(docs, is_cached):

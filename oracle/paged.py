@@ -204,6 +204,10 @@ def kv_append_image(cache, new, block_table, cu_suffix, prefix_len, block_size: 
     lands in block block_table[r, t // bs] at slot t % bs; every other
     element keeps its value.
 
+    A table entry outside [0, NB) names no block of the pool (the paper's
+    engine never produces one; the reading taken for a corrupted table is that
+    the write is dropped): those tokens change nothing.
+
     layout "slot_d": cache is [NB, Hkv, bs, D] (the K cache);
     layout "d_slot": cache is [NB, Hkv, D, bs], each block stored transposed
     (the V cache). new: [total_s, Hkv, D]; block_table: [B, stride] int;
@@ -212,13 +216,16 @@ def kv_append_image(cache, new, block_table, cu_suffix, prefix_len, block_size: 
     if layout not in ("slot_d", "d_slot"):
         raise ValueError(f"unknown layout {layout!r}")
     out = np.array(cache, copy=True)
+    nb = out.shape[0]
     new = np.asarray(new)
     bt = np.asarray(block_table)
     for r in range(len(prefix_len)):
         p = int(prefix_len[r])
         s = int(cu_suffix[r + 1]) - int(cu_suffix[r])
         t = np.arange(p, p + s)
-        blocks = bt[r, t // block_size]
+        blocks = bt[r, t // block_size].astype(np.int64)
+        keep = (blocks >= 0) & (blocks < nb)
+        t, blocks = t[keep], blocks[keep]
         slots = t % block_size
         rows = new[int(cu_suffix[r]) + (t - p)]          # [s, Hkv, D]
         if layout == "slot_d":
@@ -239,6 +246,8 @@ def kv_append_image_loops(cache, new, block_table, cu_suffix, prefix_len, block_
         for i in range(s):
             t = p + i
             blk = int(block_table[r][t // block_size])
+            if not 0 <= blk < out.shape[0]:
+                continue
             for g in range(out.shape[1]):
                 for d in range(D):
                     val = new[int(cu_suffix[r]) + i, g, d]
@@ -246,4 +255,21 @@ def kv_append_image_loops(cache, new, block_table, cu_suffix, prefix_len, block_
                         out[blk, g, t % block_size, d] = val
                     else:
                         out[blk, g, d, t % block_size] = val
+    return out
+
+
+def zero_out_of_pool_blocks(x, block_row, num_blocks: int, block_size: int = 16):
+    """Logical K (or V) rows [L, Hkv, D] of one request as attention reads them
+    through its block-table row: the rows of logical block b whose table entry
+    block_row[b] lies outside [0, num_blocks) are zeros (the reading taken for a
+    table entry that names no block of the pool: the paper's engine never
+    produces one). Every other row is unchanged. Returns a float64 copy."""
+    if hasattr(x, "detach"):
+        x = x.detach().to("cpu").double().numpy()
+    out = np.array(x, dtype=np.float64, copy=True)
+    L = out.shape[0]
+    for b in range((L + block_size - 1) // block_size):
+        blk = int(block_row[b])
+        if not 0 <= blk < num_blocks:
+            out[b * block_size:min(L, (b + 1) * block_size)] = 0.0
     return out

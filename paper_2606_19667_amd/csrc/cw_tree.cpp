@@ -9,8 +9,10 @@
 // engine did not actually reuse it. Sec. 4 and Table `baselines`: retrieval
 // order, lexicographic sorting and a recency heuristic as baselines.
 //
-// Layout: nodes live in one flat array (index 0 is the root) and a child is
-// found through an open-addressing index keyed by (parent, document). Every
+// Layout: nodes live in one flat array (index 0 is the root); a child is found
+// through an open-addressing index keyed by (parent, document), and each node
+// also lists its children (first child, next sibling) for walks that visit
+// every child of a node. Every
 // `window` insertions the nodes that left the window are dropped and both
 // arrays are rebuilt, which keeps the tree at O(window * k) nodes. A node is
 // always created after its parent and compaction keeps the order, so a
@@ -45,6 +47,8 @@ struct Node {
   int64_t last;    // clock of the latest insertion through this node
   int64_t stale;   // clock of the latest stale mark, kNever if none
   int32_t parent;
+  int32_t first_child = -1;    // children of a node form a singly linked list
+  int32_t next_sibling = -1;
 };
 
 // (parent, doc) -> node index; linear probing, capacity a power of two kept
@@ -145,6 +149,12 @@ struct cw_tree {
     kids.reset(min_entries);
     for (size_t i = 1; i < nodes.size(); ++i) kids.put(nodes[i].parent, nodes[i].doc, int32_t(i));
   }
+  // Appends node c (already in `nodes`, parent set) to its parent's child list.
+  void link_child(int32_t c) {
+    Node& p = nodes[size_t(nodes[size_t(c)].parent)];
+    nodes[size_t(c)].next_sibling = p.first_child;
+    p.first_child = c;
+  }
   // Drops every node that left the window (its subtree left with it: a
   // child's insertion clock never exceeds its parent's) and old document clocks.
   void prune() {
@@ -162,6 +172,8 @@ struct cw_tree {
       kept.push_back(y);
     }
     nodes.swap(kept);
+    for (Node& x : nodes) x.first_child = x.next_sibling = -1;
+    for (size_t i = 1; i < nodes.size(); ++i) link_child(int32_t(i));
     rebuild_index(nodes.size());
     DocClock fresh;
     fresh.reset(docs.count);
@@ -197,30 +209,46 @@ int32_t walk(const cw_tree* t, const int64_t* order, int32_t k, int32_t* probes)
   return n;
 }
 
-// Algorithm 1: from the root, place the first remaining document (in retrieval
-// rank) whose child exists and is cached; when none does, append the rest in
-// retrieval rank.
+// Greedy order (Sec. 3.3, Algorithm 1), by what each level selects: among the
+// cached children of the current node whose document is in the retrieved set
+// and not yet placed, the one of lowest retrieval rank; the run ends at a node
+// with no such child and the unplaced documents follow in retrieval rank.
+// The children are visited through the node's child list; a rank table sorted
+// by document ID maps a child's document to its rank. *probes gets the child
+// lookups a scan in retrieval rank would make for the same choices: at a level
+// that places rank j, one per unplaced rank <= j; at the level that finds
+// nothing (when documents remain), one per unplaced document.
 int32_t greedy(const cw_tree* t, const int64_t* docs, int32_t k, int64_t* out, int32_t* probes) {
-  std::vector<int64_t> rest(docs, docs + k);
-  int32_t node = 0, placed = 0;
-  while (!rest.empty()) {
-    int32_t hit = -1, hit_node = -1;
-    for (size_t j = 0; j < rest.size(); ++j) {
-      ++*probes;
-      const int32_t c = t->child(node, rest[j]);
-      if (c >= 0 && t->cached(c)) {
-        hit = int32_t(j);
-        hit_node = c;
-        break;
+  std::vector<std::pair<int64_t, int32_t>> by_doc(static_cast<size_t>(k));
+  for (int32_t j = 0; j < k; ++j) by_doc[size_t(j)] = {docs[j], j};
+  std::sort(by_doc.begin(), by_doc.end());
+  auto rank_of = [&](int64_t d) -> int32_t {
+    auto it = std::lower_bound(by_doc.begin(), by_doc.end(), std::make_pair(d, int32_t(-1)));
+    return (it != by_doc.end() && it->first == d) ? it->second : -1;
+  };
+  std::vector<char> placed(static_cast<size_t>(k), 0);
+  int32_t node = 0, depth = 0;
+  while (depth < k) {
+    int32_t best = k, best_node = -1;
+    for (int32_t c = t->nodes[size_t(node)].first_child; c >= 0; c = t->nodes[size_t(c)].next_sibling) {
+      if (!t->cached(c)) continue;
+      const int32_t j = rank_of(t->nodes[size_t(c)].doc);
+      if (j >= 0 && j < best && !placed[size_t(j)]) {
+        best = j;
+        best_node = c;
       }
     }
-    if (hit < 0) break;
-    out[placed++] = rest[size_t(hit)];
-    rest.erase(rest.begin() + hit);
-    node = hit_node;
+    int32_t scanned = 0;   // unplaced ranks up to the pick (all of them when none)
+    for (int32_t j = 0; j < k && j <= best; ++j) scanned += placed[size_t(j)] ? 0 : 1;
+    *probes += scanned;
+    if (best_node < 0) break;
+    placed[size_t(best)] = 1;
+    out[depth++] = docs[best];
+    node = best_node;
   }
-  const int32_t depth = placed;
-  for (int64_t d : rest) out[placed++] = d;
+  int32_t n = depth;
+  for (int32_t j = 0; j < k; ++j)
+    if (!placed[size_t(j)]) out[n++] = docs[j];
   return depth;
 }
 
@@ -315,6 +343,7 @@ extern "C" cw_status cw_tree_insert(cw_tree* tree, const int64_t* order, int32_t
       tree->reserve_child();
       c = int32_t(tree->nodes.size());
       tree->nodes.push_back(Node{order[j], now, kNever, node});
+      tree->link_child(c);
       tree->kids.put(node, order[j], c);
     }
     tree->nodes[size_t(c)].last = now;

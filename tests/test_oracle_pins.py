@@ -418,3 +418,47 @@ def test_append_image_layouts_are_transposes():
     a = paged.kv_append_image(cache, new, bt, cu, P, 4)
     b = paged.kv_append_image(cache.swapaxes(2, 3), new, bt, cu, P, 4, layout="d_slot")
     assert np.array_equal(a.swapaxes(2, 3), b)
+
+
+# ---------------------------------------------------------------- out-of-pool table entries
+def test_append_image_drops_out_of_pool_writes():
+    """A block-table entry outside [0, NB) names no block: its tokens write
+    nothing (hand example: entry -1 and entry NB in one row)."""
+    cache = np.full((4, 1, 4, 2), 7, dtype=np.uint16)
+    new = np.arange(1, 1 + 9 * 2, dtype=np.uint16).reshape(9, 1, 2)
+    bt = np.array([[2, -1, 4]], dtype=np.int32)      # tokens 0..3 -> 2, 4..7 dropped, 8 dropped
+    for layout, c in (("slot_d", cache), ("d_slot", cache.swapaxes(2, 3).copy())):
+        out = paged.kv_append_image(c, new, bt, [0, 9], [0], block_size=4, layout=layout)
+        ref = paged.kv_append_image_loops(c, new, bt, [0, 9], [0], block_size=4, layout=layout)
+        assert np.array_equal(out, ref)
+        blk2 = out[2, 0] if layout == "slot_d" else out[2, 0].T
+        assert blk2.tolist() == [[1, 2], [3, 4], [5, 6], [7, 8]]
+        for b in (0, 1, 3):                         # untouched, including the last block (-1 must not wrap)
+            assert (out[b] == 7).all()
+
+
+def test_zero_out_of_pool_blocks_hand_example():
+    x = np.arange(1, 1 + 11 * 2, dtype=np.float64).reshape(11, 1, 2)   # L = 11, blocks of 4: 3 blocks
+    row = np.array([5, -1, 6, 0])                   # NB = 6: block 0 ok, 1 out (-1), 2 out (== NB)
+    out = paged.zero_out_of_pool_blocks(x, row, num_blocks=6, block_size=4)
+    assert np.array_equal(out[0:4], x[0:4])
+    assert (out[4:11] == 0).all()
+    out2 = paged.zero_out_of_pool_blocks(x, [0, 1, 2], num_blocks=3, block_size=4)
+    assert np.array_equal(out2, x)
+
+
+def test_out_of_pool_prefix_block_is_a_zero_key_in_the_softmax():
+    """Reading of an out-of-pool prefix block: 16 keys of zeros and values of
+    zeros, which get weight exp(0) before normalisation. Closed form with the
+    other keys' values constant c: O = c * Z_rest / (Z_rest + 16)."""
+    rng = np.random.default_rng(3)
+    P, S, D, bs = 32, 3, 8, 16
+    q = rng.standard_normal((S, 1, D))
+    k = rng.standard_normal((P + S, 1, D))
+    v = np.full((P + S, 1, D), 2.5)
+    kz = paged.zero_out_of_pool_blocks(k, [-1, 0, 1], num_blocks=4, block_size=bs)
+    vz = paged.zero_out_of_pool_blocks(v, [-1, 0, 1], num_blocks=4, block_size=bs)
+    out = A.suffix_prefill_attention(q, kz, vz, P, 0.5)
+    for i in range(S):
+        z_rest = np.exp(0.5 * (k[bs:P + i + 1, 0] @ q[i, 0])).sum()
+        assert np.allclose(out[i, 0], 2.5 * z_rest / (z_rest + bs), rtol=1e-12, atol=0)
