@@ -101,13 +101,14 @@ def make_workload(name: str, seed: int):
 
 
 def executed_mfma_flops(cu_suffix, prefix_len, hq: int, hkv: int, D: int) -> int:
-    """MFMA FLOPs the attention kernel executes: every tile of the plan runs
-    `cost` 64-key steps over all 256 packed rows (QK^T and PV), masked keys and
-    padding rows included. Divided by the algorithmic FLOPs this is the
-    masked-tile waste factor."""
+    """MFMA FLOPs the attention kernel executes: every entry of the plan runs
+    its 64-key steps [kbeg, kend) over all 256 packed rows (QK^T and PV),
+    masked keys and padding rows included. Divided by the algorithmic FLOPs
+    this is the masked-tile waste factor."""
     from paper_2606_19667_amd import cw
-    plan, n = cw.suffix_prefill_plan(cu_suffix, prefix_len, hq, hkv, D)
-    steps = int(plan.reshape(-1, 4)[:n, 3][plan.reshape(-1, 4)[:n, 0] >= 0].astype(np.int64).sum())
+    ents = cw.plan_entries(cw.suffix_prefill_plan(cu_suffix, prefix_len, hq, hkv, D))
+    real = ents[:, cw.ENT_R] >= 0
+    steps = int((ents[real, cw.ENT_KEND] - ents[real, cw.ENT_KBEG]).astype(np.int64).sum())
     return steps * 256 * 64 * D * 4
 
 

@@ -54,7 +54,7 @@ typedef int32_t cw_status;
 #define CW_ENOSPC (-3)       /* block pool exhausted */
 #define CW_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
 
-#define CW_ABI_VERSION 2
+#define CW_ABI_VERSION 3
 
 /* ABI version of the loaded library (CW_ABI_VERSION at build time). */
 int32_t cw_abi_version(void);
@@ -229,8 +229,8 @@ cw_status cw_tree_order(const cw_tree* tree, int32_t strategy, const int64_t* do
  * For every request r and token t in [P_r, L_r):
  *   k_cache[block_table[r, t / bs], h, t % bs, :] = k_new[cu[r] + t - P_r, h, :]
  *   v_cache[block_table[r, t / bs], h, :, t % bs] = v_new[cu[r] + t - P_r, h, :]
- * a bit copy. Nothing else in the caches changes. A block
- * ID outside [0, num_blocks) drops the write (never faults).
+ * a bit copy. Nothing else in the caches changes. A table entry outside
+ * [0, num_blocks) drops the writes of its tokens (never a fault).
  *   cu_suffix_dev / prefix_len_dev   device copies read by the kernel
  *   cu_suffix_host / prefix_len_host host copies used for validation and
  *                                    launch sizing; must hold the same values
@@ -246,27 +246,45 @@ cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_cache, void
                        int32_t block_size, int32_t num_blocks, void* stream);
 
 /* ------------------------------------------------------------------------
- * Host: tile schedule for cw_suffix_prefill_attn.
+ * Host: work plan for cw_suffix_prefill_attn and cw_suffix_prefill_attn_split
+ * (paper Sec. 1 and 2.1: after the prefix match, each request r has P_r cached
+ * prefix tokens and S_r suffix rows to prefill; the plan is how that ragged
+ * work is cut into tiles and spread over the GPU).
  *
  * The attention kernel works on tiles of (request, KV head, run of
- * 256 / (Hq / Hkv) suffix rows), i.e. 256 packed (query head, row) pairs;
- * the plan lists them heaviest first and groups the tiles of one
- * (request, KV head) on one L2 partition. A plan depends only on the batch
- * shape, so one plan serves every layer of a model for that batch.
+ * 256 / (Hq / Hkv) suffix rows), i.e. 256 packed (query head, row) pairs whose
+ * keys run from position 0 to the last row's position, in steps of 64 keys.
+ * num_splits > 1 cuts each tile's steps into that many runs (the split path);
+ * each run is one plan entry. The grid is persistent (at most one workgroup
+ * per CU, 256 on MI355X): entries are spread over per-workgroup queues, longest
+ * work first, with the tiles of one (request, KV head) kept on one L2
+ * partition where the batch allows. A plan depends only on the batch
+ * description (cu_suffix, prefix_len, heads, head_dim, num_splits), so one plan
+ * serves every layer of a model for that batch.
  *
- * cw_suffix_prefill_plan_words returns the int32 capacity a plan needs (or a
+ * Layout: a 16-word header (magic, entry count, a 64-bit fingerprint of the
+ * batch description, grid, split count, batch, heads, head_dim, rows, queue
+ * length, work), then 16-word entries, each with a check word. The device
+ * calls take the host copy (plan_host: they validate its header against their
+ * own host batch description, so a plan built for another batch is refused
+ * with CW_EINVAL) and a device copy of the whole plan (plan_dev: the kernels
+ * compute nothing for a device plan whose header fingerprint differs, and stop
+ * a queue at an entry whose check word does not match).
+ *
+ * cw_suffix_prefill_plan_words returns the int32 words a plan needs (or a
  * negative cw_status). cw_suffix_prefill_plan writes it:
- *   plan_host       host int32 [plan_words]; copy it to device memory unchanged
- *   out_num_tiles   number of tile entries to pass to cw_suffix_prefill_attn
- * CW_EINVAL / CW_EUNSUPPORTED as for cw_suffix_prefill_attn; CW_EINVAL if
- * plan_words is too small. */
+ *   plan_host    host int32 [plan_words]; copy all of it to device memory
+ *   num_splits   1 .. 64 (1 for cw_suffix_prefill_attn)
+ * CW_EINVAL: NULL pointers, batch < 1, Hq % Hkv != 0, cu not non-decreasing
+ * from 0, P_r < 0, num_splits out of range, plan_words too small.
+ * CW_EUNSUPPORTED: head_dim not 64/128, Hq / Hkv > 128, too many entries. */
 int64_t cw_suffix_prefill_plan_words(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                      int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
-                                     int32_t head_dim);
+                                     int32_t head_dim, int32_t num_splits);
 cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                  int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
-                                 int32_t head_dim, int32_t* plan_host, int64_t plan_words,
-                                 int32_t* out_num_tiles);
+                                 int32_t head_dim, int32_t num_splits, int32_t* plan_host,
+                                 int64_t plan_words);
 
 /* ------------------------------------------------------------------------
  * Device: causal prefill attention of the suffix rows over the paged prefix
@@ -280,13 +298,15 @@ cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* p
  *   out[cu[r] + i, h, :] = sum_j softmax(s)_j * V_r[j, g, :]
  * bf16 inputs, fp32 accumulation and softmax, bf16 output (round to nearest
  * even). The caches must already hold the prefix and (after cw_kv_append) the
- * suffix. Block IDs outside [0, num_blocks) read as zeros (never fault).
- *   plan_dev    device copy of a plan from cw_suffix_prefill_plan for the same
- *               cu_suffix / prefix_len / heads / head_dim
- *   num_tiles   its out_num_tiles
+ * suffix. A table entry outside [0, num_blocks) (within the prompt's blocks)
+ * is read as a block of zero keys and values: never a fault, but each of its
+ * keys enters the softmax with score 0 and value 0.
+ *   plan_host   the plan from cw_suffix_prefill_plan for this batch with
+ *               num_splits = 1 (host memory; its header is read)
+ *   plan_dev    a device copy of the whole plan
  * CW_EINVAL: NULL pointer, batch < 1, Hq % Hkv != 0, P_r % bs != 0, cu not
- * non-decreasing from 0, ceil(L_r / bs) > bt_stride, num_tiles not matching the
- * shape, softmax_scale not finite and positive.
+ * non-decreasing from 0, ceil(L_r / bs) > bt_stride, softmax_scale not finite
+ * and positive, a plan built for another batch description or with splits.
  * CW_EUNSUPPORTED: head_dim not 64/128, block_size != 16, Hq / Hkv > 128.
  * CW_EHIP: launch failure. */
 cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void* v_cache,
@@ -295,27 +315,25 @@ cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void*
                                  const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                  int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                  int32_t head_dim, int32_t block_size, int32_t num_blocks,
-                                 float softmax_scale, const int32_t* plan_dev, int32_t num_tiles,
+                                 float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev,
                                  void* out, void* stream);
 
 /* ------------------------------------------------------------------------
  * Device: split-KV variant of cw_suffix_prefill_attn, for batches with few
  * tiles (short suffixes such as a question after a fully cached evidence
  * prefix: paper Sec. 1 and 3.3, the reuse the ordering aims for). Same result
- * up to rounding, same arguments and plan.
+ * up to rounding, same arguments, with a plan built for num_splits runs.
  *
- * Each plan tile's key range is divided into num_splits runs of whole 64-key
- * steps, processed by separate workgroups; each run's attention over its own
- * keys (normalised O in fp32 and its base-2 log-sum-exp per row) is written to
- * `workspace`, then combined exactly as by cw_lse_merge into out (bf16).
- *   num_splits       1 .. 64
+ * Each tile's key range is divided into num_splits runs of whole 64-key steps
+ * (the plan's entries); each run's attention over its own keys (normalised O
+ * in fp32 and its base-2 log-sum-exp per row) is written to `workspace`, then
+ * combined exactly as by cw_lse_merge into out (bf16).
  *   workspace        caller-owned device memory of at least
  *                    cw_suffix_prefill_split_workspace_bytes(total_s, Hq, D,
  *                    num_splits) bytes; overwritten by the call
- * Errors as cw_suffix_prefill_attn, plus CW_EINVAL for num_splits out of range
- * or a missing / too small workspace.
- * cw_suffix_prefill_split_workspace_bytes returns the size, or a negative
- * cw_status for invalid arguments. */
+ * Errors as cw_suffix_prefill_attn, plus CW_EINVAL for a missing / too small
+ * workspace. cw_suffix_prefill_split_workspace_bytes returns the size, or a
+ * negative cw_status for invalid arguments (num_splits outside 1 .. 64). */
 int64_t cw_suffix_prefill_split_workspace_bytes(int64_t total_rows, int32_t num_q_heads, int32_t head_dim,
                                                 int32_t num_splits);
 cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_cache, const void* v_cache,
@@ -324,9 +342,8 @@ cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_cache, const
                                        const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                        int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                        int32_t head_dim, int32_t block_size, int32_t num_blocks,
-                                       float softmax_scale, const int32_t* plan_dev, int32_t num_tiles,
-                                       int32_t num_splits, void* workspace, int64_t workspace_bytes,
-                                       void* out, void* stream);
+                                       float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev,
+                                       void* workspace, int64_t workspace_bytes, void* out, void* stream);
 
 /* ------------------------------------------------------------------------
  * Device: merge of attention results computed over disjoint key sets (the

@@ -559,167 +559,256 @@ extern "C" cw_status cw_release_batch(cw_pool* pool, const int32_t* block_table,
 }
 
 // ---------------------------------------------------------------------------
-// Tile planner. A tile is (request, KV head, first suffix row); its cost is the
-// number of KV tiles its rows visit under the causal limit. Tiles are listed
-// heaviest first; when there are enough (request, KV head) pairs, each pair is
-// pinned to one L2 partition (pairs balanced by total cost) so the tiles that
-// re-read a pair's K/V share that partition's L2, and the per-partition queues
-// are interleaved so that workgroup i lands on partition i % 8. Empty entries
-// (request -1) pad the shorter queues.
+// Attention planner. A tile is (request, KV head, first suffix row): 256
+// packed (query head, row) pairs whose keys run from 0 to the last row's
+// position; its key range is cut into num_splits runs of whole 64-key steps
+// (one run when not splitting), and each run is one plan entry. The attention
+// grid is persistent, one workgroup per CU; workgroup w runs entries w,
+// w + grid, w + 2 grid, ... of its queue.
+//
+// Queues are filled longest-processing-time first (each entry, heaviest first,
+// goes to the queue with the least work so far), so the queues end together.
+// With enough (request, KV head) pairs and 256 queues, the pairs are first
+// spread over the eight L2 partitions (queue w runs on partition w % 8) by
+// total work, so every tile re-reading a pair's K/V hits that partition's L2;
+// the entries of a partition then fill its 32 queues.
 // ---------------------------------------------------------------------------
 namespace {
 
 cw_status plan_args(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv,
-                    int32_t d) {
+                    int32_t d, int32_t splits) {
   if (!cu || !plen) return fail(CW_EINVAL, "cu_suffix_host and prefix_len_host are required");
   if (batch < 1) return fail(CW_EINVAL, "batch must be >= 1");
   if (hq < 1 || hkv < 1 || hq % hkv != 0)
     return fail(CW_EINVAL, "num_q_heads must be a positive multiple of num_kv_heads");
   if (hq / hkv > cw::kMaxGroup) return fail(CW_EUNSUPPORTED, "more than 128 query heads per KV head");
   if (d != 64 && d != 128) return fail(CW_EUNSUPPORTED, "head_dim must be 64 or 128");
+  if (splits < 1 || splits > cw::kMaxSplits) return fail(CW_EINVAL, "num_splits must be in [1, 64]");
   if (cu[0] != 0) return fail(CW_EINVAL, "cu_suffix[0] must be 0");
   for (int32_t r = 0; r < batch; ++r) {
     if (cu[r + 1] < cu[r]) return fail(CW_EINVAL, "cu_suffix must be non-decreasing");
     if (plen[r] < 0) return fail(CW_EINVAL, "prefix_len must be >= 0");
+    if (int64_t(plen[r]) + (cu[r + 1] - cu[r]) > INT32_MAX - cw::kKvTile)
+      return fail(CW_EUNSUPPORTED, "prompt too long");
   }
   return CW_OK;
 }
 
-inline int32_t tile_cost(int32_t P, int32_t row0, int32_t S, int32_t per) {
-  const int64_t kv_end = int64_t(P) + row0 + std::min(per, S - row0);
-  return int32_t((kv_end + cw::kKvTile - 1) / cw::kKvTile);
-}
-
-// Which partition queue each (request, KV head) pair feeds (-1: one plain
-// queue) and the padded plan length.
-struct PlanShape {
-  int32_t per = 0;
-  int64_t tiles = 0;
-  int64_t padded = 0;
-  int32_t max_cost = 0;
-  std::vector<int8_t> part;  // [batch * hkv], empty when not grouped
+struct Entry {
+  int32_t f[cw::kEntFields];
+  int64_t cost;
+  int32_t pair;
 };
 
-PlanShape plan_shape(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv) {
-  PlanShape ps;
-  ps.per = cw::tile_positions(hq / hkv);
-  std::vector<int64_t> req_cost(size_t(batch), 0), req_count(size_t(batch), 0);
-  int64_t total = 0;
+// Work of an entry in 64-key steps, plus a step's worth for its start and end.
+constexpr int64_t kEntryOverhead = 1;
+
+std::vector<Entry> plan_entries(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv,
+                                int32_t splits) {
+  const int32_t per = cw::tile_positions(hq / hkv);
+  std::vector<Entry> out;
   for (int32_t r = 0; r < batch; ++r) {
-    const int32_t S = cu[r + 1] - cu[r];
-    for (int32_t row0 = 0; row0 < S; row0 += ps.per) {
-      const int32_t c = tile_cost(plen[r], row0, S, ps.per);
-      req_cost[size_t(r)] += c;
-      req_count[size_t(r)] += 1;
-      ps.max_cost = std::max(ps.max_cost, c);
+    const int32_t S = cu[r + 1] - cu[r], P = plen[r];
+    for (int32_t row0 = 0; row0 < S; row0 += per) {
+      const int32_t nvalid = std::min(per, S - row0);
+      const int32_t n = int32_t((int64_t(P) + row0 + nvalid + cw::kKvTile - 1) / cw::kKvTile);
+      const int32_t run = (n + splits - 1) / splits;
+      for (int32_t g = 0; g < hkv; ++g)
+        for (int32_t s = 0; s < splits; ++s) {
+          Entry e;
+          const int32_t kb = std::min(n, s * run), ke = std::min(n, kb + run);
+          const int32_t f[cw::kEntFields] = {r, g, row0, nvalid, cu[r], P, P + S, kb, ke, s};
+          std::copy(f, f + cw::kEntFields, e.f);
+          e.cost = (ke - kb) + (ke > kb ? kEntryOverhead : 0);
+          e.pair = r * hkv + g;
+          out.push_back(e);
+        }
     }
-    ps.tiles += req_count[size_t(r)] * hkv;
-    total += req_cost[size_t(r)] * hkv;
   }
-  ps.padded = ps.tiles;
+  return out;
+}
+
+// Queue of every entry and the queue count.
+struct Queues {
+  int32_t grid = 0;
+  int32_t len = 0;                       // entries of the longest queue
+  std::vector<std::vector<int32_t>> q;   // entry indices per queue, in run order
+};
+
+// Longest processing time first over `n` queues.
+void lpt(const std::vector<Entry>& ents, std::vector<int32_t> idx, const std::vector<int32_t>& queues,
+         std::vector<std::vector<int32_t>>* q) {
+  std::stable_sort(idx.begin(), idx.end(), [&](int32_t a, int32_t b) { return ents[size_t(a)].cost > ents[size_t(b)].cost; });
+  std::vector<int64_t> load(queues.size(), 0);
+  for (int32_t i : idx) {
+    size_t x = 0;
+    for (size_t k = 1; k < queues.size(); ++k)
+      if (load[k] < load[x]) x = k;
+    load[x] += ents[size_t(i)].cost;
+    (*q)[size_t(queues[x])].push_back(i);
+  }
+}
+
+Queues plan_queues(const std::vector<Entry>& ents, int32_t batch, int32_t hkv) {
+  Queues qs;
+  qs.grid = int32_t(std::min<size_t>(ents.size(), cw::kNumCu));
+  if (qs.grid == 0) return qs;
+  qs.q.assign(size_t(qs.grid), {});
+  std::vector<int32_t> all(ents.size());
+  std::iota(all.begin(), all.end(), 0);
   const int64_t npairs = int64_t(batch) * hkv;
-  if (npairs < 4 * cw::kNumXcd) return ps;
-  std::vector<int32_t> order(static_cast<size_t>(batch));
-  std::iota(order.begin(), order.end(), 0);
-  std::stable_sort(order.begin(), order.end(),
-                   [&](int32_t a, int32_t b) { return req_cost[size_t(a)] > req_cost[size_t(b)]; });
-  std::vector<int8_t> part(size_t(npairs), 0);
-  int64_t load[cw::kNumXcd] = {0};
-  int64_t len[cw::kNumXcd] = {0};
-  for (int32_t r : order)
-    for (int32_t g = 0; g < hkv; ++g) {
+  bool grouped = false;
+  if (qs.grid == cw::kNumCu && npairs >= 4 * cw::kNumXcd) {
+    // pairs to partitions by total work, heaviest pair first
+    std::vector<int64_t> pair_cost(size_t(npairs), 0);
+    for (const Entry& e : ents) pair_cost[size_t(e.pair)] += e.cost;
+    std::vector<int32_t> order(static_cast<size_t>(npairs));
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int32_t a, int32_t b) { return pair_cost[size_t(a)] > pair_cost[size_t(b)]; });
+    std::vector<int8_t> part(size_t(npairs), 0);
+    int64_t load[cw::kNumXcd] = {0};
+    int64_t total = 0;
+    for (int32_t pr : order) {
       int x = 0;
       for (int i = 1; i < cw::kNumXcd; ++i)
         if (load[i] < load[x]) x = i;
-      part[size_t(int64_t(r) * hkv + g)] = int8_t(x);
-      load[x] += req_cost[size_t(r)];
-      len[x] += req_count[size_t(r)];
+      part[size_t(pr)] = int8_t(x);
+      load[x] += pair_cost[size_t(pr)];
+      total += pair_cost[size_t(pr)];
     }
-  const int64_t max_load = *std::max_element(load, load + cw::kNumXcd);
-  if (max_load * cw::kNumXcd > total + total / 20) return ps;  // >5% imbalance: one plain queue
-  ps.part = std::move(part);
-  ps.padded = *std::max_element(len, len + cw::kNumXcd) * cw::kNumXcd;
-  return ps;
-}
-
-// Writes the plan: 4 int32 per entry {request, kv head, first row, cost}.
-void write_plan(const PlanShape& ps, const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hkv,
-                int32_t* out) {
-  for (int64_t e = 0; e < ps.padded; ++e) {
-    out[4 * e + 0] = -1;
-    out[4 * e + 1] = 0;
-    out[4 * e + 2] = 0;
-    out[4 * e + 3] = 0;
-  }
-  auto put = [&](int64_t e, int32_t r, int32_t g, int32_t row0) {
-    out[4 * e + 0] = r;
-    out[4 * e + 1] = g;
-    out[4 * e + 2] = row0;
-    out[4 * e + 3] = tile_cost(plen[r], row0, cu[r + 1] - cu[r], ps.per);
-  };
-  if (ps.part.empty()) {
-    // One queue, heaviest first: counting sort by cost; ties keep generation
-    // order (request, first row, KV head).
-    const int32_t nc = ps.max_cost + 1;
-    std::vector<int64_t> start(size_t(nc) + 1, 0);
-    for (int32_t r = 0; r < batch; ++r)
-      for (int32_t row0 = 0, S = cu[r + 1] - cu[r]; row0 < S; row0 += ps.per)
-        start[size_t(nc - 1 - tile_cost(plen[r], row0, S, ps.per)) + 1] += hkv;
-    for (int32_t k = 0; k < nc; ++k) start[size_t(k) + 1] += start[size_t(k)];
-    for (int32_t r = 0; r < batch; ++r)
-      for (int32_t row0 = 0, S = cu[r + 1] - cu[r]; row0 < S; row0 += ps.per) {
-        int64_t& pos = start[size_t(nc - 1 - tile_cost(plen[r], row0, S, ps.per))];
-        for (int32_t g = 0; g < hkv; ++g) put(pos++, r, g, row0);
+    const int64_t max_load = *std::max_element(load, load + cw::kNumXcd);
+    if (max_load * cw::kNumXcd <= total + total / 50) {   // within 2% of even
+      grouped = true;
+      for (int x = 0; x < cw::kNumXcd; ++x) {
+        std::vector<int32_t> idx, queues;
+        for (int32_t i : all)
+          if (part[size_t(ents[size_t(i)].pair)] == x) idx.push_back(i);
+        for (int32_t w = x; w < qs.grid; w += cw::kNumXcd) queues.push_back(w);
+        lpt(ents, idx, queues, &qs.q);
       }
-    return;
-  }
-  // One queue per L2 partition, pair-major: the partition's (request, KV head)
-  // pairs by total cost (heaviest first), each pair's tiles heaviest (last rows)
-  // first. Only a few pairs are in flight per partition at a time, so their K/V
-  // stay in that partition's L2. Queue x, position i -> entry i * 8 + x.
-  std::vector<int64_t> req_cost(size_t(batch), 0);
-  for (int32_t r = 0; r < batch; ++r)
-    for (int32_t row0 = 0, S = cu[r + 1] - cu[r]; row0 < S; row0 += ps.per)
-      req_cost[size_t(r)] += tile_cost(plen[r], row0, S, ps.per);
-  std::vector<int32_t> order(static_cast<size_t>(batch));
-  std::iota(order.begin(), order.end(), 0);
-  std::stable_sort(order.begin(), order.end(),
-                   [&](int32_t a, int32_t b) { return req_cost[size_t(a)] > req_cost[size_t(b)]; });
-  int64_t pos[cw::kNumXcd] = {0};
-  for (int32_t r : order)
-    for (int32_t g = 0; g < hkv; ++g) {
-      const int x = ps.part[size_t(int64_t(r) * hkv + g)];
-      const int32_t S = cu[r + 1] - cu[r];
-      if (S == 0) continue;
-      const int32_t last = ((S - 1) / ps.per) * ps.per;
-      for (int32_t row0 = last; row0 >= 0; row0 -= ps.per) put(pos[x]++ * cw::kNumXcd + x, r, g, row0);
     }
+  }
+  if (!grouped) {
+    std::vector<int32_t> queues(size_t(qs.grid));
+    std::iota(queues.begin(), queues.end(), 0);
+    lpt(ents, all, queues, &qs.q);
+  }
+  for (const auto& v : qs.q) qs.len = std::max<int32_t>(qs.len, int32_t(v.size()));
+  return qs;
 }
 
 }  // namespace
 
+namespace cw {
+uint64_t batch_fingerprint(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv,
+                           int32_t d, int32_t splits) {
+  // FNV-1a over the little-endian words of the description, then a final mix
+  uint64_t h = 0xcbf29ce484222325ULL;
+  auto add = [&](uint32_t w) {
+    for (int i = 0; i < 4; ++i) {
+      h ^= (w >> (8 * i)) & 0xFFu;
+      h *= 0x100000001b3ULL;
+    }
+  };
+  add(uint32_t(batch));
+  add(uint32_t(hq));
+  add(uint32_t(hkv));
+  add(uint32_t(d));
+  add(uint32_t(splits));
+  for (int32_t r = 0; r <= batch; ++r) add(uint32_t(cu[r]));
+  for (int32_t r = 0; r < batch; ++r) add(uint32_t(plen[r]));
+  h ^= h >> 33;
+  h *= 0xff51afd7ed558ccdULL;
+  h ^= h >> 33;
+  return h;
+}
+}  // namespace cw
+
 extern "C" int64_t cw_suffix_prefill_plan_words(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                                 int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
-                                                int32_t head_dim) {
-  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim);
+                                                int32_t head_dim, int32_t num_splits) {
+  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim, num_splits);
   if (st != CW_OK) return st;
-  const PlanShape ps = plan_shape(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads);
+  const std::vector<Entry> ents = plan_entries(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
+                                               num_splits);
+  const Queues qs = plan_queues(ents, batch, num_kv_heads);
   cw::ok();
-  return 4 * ps.padded;
+  return cw::kPlanHeaderWords + int64_t(cw::kPlanEntryWords) * qs.grid * qs.len;
 }
 
 extern "C" cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                             int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
-                                            int32_t head_dim, int32_t* plan_host, int64_t plan_words,
-                                            int32_t* out_num_tiles) {
-  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim);
+                                            int32_t head_dim, int32_t num_splits, int32_t* plan_host,
+                                            int64_t plan_words) {
+  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim, num_splits);
   if (st != CW_OK) return st;
-  if (!out_num_tiles) return fail(CW_EINVAL, "out_num_tiles is required");
-  const PlanShape ps = plan_shape(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads);
-  if (ps.padded > INT32_MAX) return fail(CW_EUNSUPPORTED, "too many tiles");
-  if (4 * ps.padded > plan_words || (!plan_host && ps.padded > 0))
-    return fail(CW_EINVAL, "plan buffer too small: need " + std::to_string(4 * ps.padded) + " words");
-  write_plan(ps, cu_suffix_host, prefix_len_host, batch, num_kv_heads, plan_host);
-  *out_num_tiles = int32_t(ps.padded);
+  const std::vector<Entry> ents = plan_entries(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
+                                               num_splits);
+  const Queues qs = plan_queues(ents, batch, num_kv_heads);
+  const int64_t padded = int64_t(qs.grid) * qs.len;
+  const int64_t need = cw::kPlanHeaderWords + cw::kPlanEntryWords * padded;
+  if (padded > INT32_MAX / cw::kPlanEntryWords) return fail(CW_EUNSUPPORTED, "too many plan entries");
+  if (!plan_host || plan_words < need)
+    return fail(CW_EINVAL, "plan buffer too small: need " + std::to_string(need) + " words");
+  const uint64_t fp = cw::batch_fingerprint(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
+                                            head_dim, num_splits);
+  const uint32_t lo = uint32_t(fp), hi = uint32_t(fp >> 32);
+  int64_t work = 0;
+  for (const Entry& e : ents) work += e.cost;
+  std::fill(plan_host, plan_host + need, 0);
+  int32_t* h = plan_host;
+  h[cw::kHdrMagic] = cw::kPlanMagic;
+  h[cw::kHdrEntries] = int32_t(padded);
+  h[cw::kHdrFpLo] = int32_t(lo);
+  h[cw::kHdrFpHi] = int32_t(hi);
+  h[cw::kHdrGrid] = qs.grid;
+  h[cw::kHdrSplits] = num_splits;
+  h[cw::kHdrBatch] = batch;
+  h[cw::kHdrHq] = num_q_heads;
+  h[cw::kHdrHkv] = num_kv_heads;
+  h[cw::kHdrD] = head_dim;
+  h[cw::kHdrRows] = cu_suffix_host[batch];
+  h[cw::kHdrQueueLen] = qs.len;
+  h[cw::kHdrWork] = int32_t(std::min<int64_t>(work, INT32_MAX));
+  int32_t* body = plan_host + cw::kPlanHeaderWords;
+  for (int32_t w = 0; w < qs.grid; ++w)
+    for (int32_t i = 0; i < qs.len; ++i) {
+      int32_t* out = body + (int64_t(i) * qs.grid + w) * cw::kPlanEntryWords;
+      if (i < int32_t(qs.q[size_t(w)].size())) {
+        const Entry& e = ents[size_t(qs.q[size_t(w)][size_t(i)])];
+        std::copy(e.f, e.f + cw::kEntFields, out);
+      } else {
+        out[cw::kEntR] = -1;   // end of this queue
+      }
+      out[cw::kEntCheck] = int32_t(cw::entry_check(lo, hi, out));
+    }
   return cw::ok();
 }
+
+// Validates a plan's header against the batch description of a device call;
+// sets the launch grid and split count.
+namespace cw {
+cw_status check_plan_header(const char* what, const int32_t* plan_host, const int32_t* cu, const int32_t* plen,
+                            int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t* grid, int32_t* splits,
+                            uint32_t* fp_lo, uint32_t* fp_hi, int32_t* num_entries) {
+  const std::string w(what);
+  if (!plan_host) return fail(CW_EINVAL, w + ": plan_host is required");
+  if (plan_host[kHdrMagic] != kPlanMagic) return fail(CW_EINVAL, w + ": plan_host is not a plan of this library");
+  const int32_t s = plan_host[kHdrSplits];
+  if (s < 1 || s > kMaxSplits) return fail(CW_EINVAL, w + ": plan has an invalid split count");
+  const uint64_t fp = batch_fingerprint(cu, plen, batch, hq, hkv, d, s);
+  if (uint32_t(plan_host[kHdrFpLo]) != uint32_t(fp) || uint32_t(plan_host[kHdrFpHi]) != uint32_t(fp >> 32) ||
+      plan_host[kHdrBatch] != batch || plan_host[kHdrHq] != hq || plan_host[kHdrHkv] != hkv || plan_host[kHdrD] != d)
+    return fail(CW_EINVAL, w + ": the plan was built for another batch (cu_suffix, prefix_len, heads or head_dim differ)");
+  const int32_t g = plan_host[kHdrGrid], len = plan_host[kHdrQueueLen], n = plan_host[kHdrEntries];
+  if (g < 0 || g > kNumCu || len < 0 || int64_t(g) * len != n)
+    return fail(CW_EINVAL, w + ": plan header is inconsistent");
+  *grid = g;
+  *splits = s;
+  *fp_lo = uint32_t(fp);
+  *fp_hi = uint32_t(fp >> 32);
+  *num_entries = n;
+  return CW_OK;
+}
+}  // namespace cw

@@ -4,6 +4,11 @@
 #include <cstdint>
 #include <string>
 
+#ifndef __HIPCC__
+#define __host__
+#define __device__
+#endif
+
 #include "cw.h"
 
 namespace cw {
@@ -20,8 +25,40 @@ constexpr int kKvTile = 64;      // keys staged in LDS per step
 constexpr int kNumXcd = 8;       // L2 partitions; workgroup i runs on partition i % 8
 constexpr int kMaxGroup = 128;   // query heads per KV head supported
 
+constexpr int kNumCu = 256;      // compute units: the attention grid's persistent workgroups
+constexpr int kMaxSplits = 64;   // key runs per tile on the split path
+
 // Suffix positions covered by one tile for a GQA group of `group` query heads.
 inline int tile_positions(int group) { return kTileRows / group; }
+
+// Attention plan layout (int32 words), written by cw_suffix_prefill_plan and
+// read by the attention kernels: a header, then entries of kPlanEntryWords.
+constexpr int kPlanHeaderWords = 16;
+constexpr int kPlanEntryWords = 16;
+constexpr int32_t kPlanMagic = 0x33505743;   // "CWP3"
+// header words
+constexpr int kHdrMagic = 0, kHdrEntries = 1, kHdrFpLo = 2, kHdrFpHi = 3, kHdrGrid = 4, kHdrSplits = 5,
+              kHdrBatch = 6, kHdrHq = 7, kHdrHkv = 8, kHdrD = 9, kHdrRows = 10, kHdrQueueLen = 11,
+              kHdrWork = 12;
+// entry words: request (-1 ends a queue), KV head, first suffix row, rows,
+// the request's first row in q/out, its prefix and prompt lengths, the run of
+// 64-key steps [kbeg, kend), the run's index, and a check word
+constexpr int kEntR = 0, kEntG = 1, kEntRow0 = 2, kEntNvalid = 3, kEntCu0 = 4, kEntP = 5, kEntL = 6,
+              kEntKbeg = 7, kEntKend = 8, kEntSplit = 9, kEntCheck = 15;
+constexpr int kEntFields = 10;   // words covered by the check word
+
+// Check word of a plan entry: a multiplicative hash of its fields seeded with
+// the batch fingerprint (the kernels recompute it; an entry that does not
+// match ends the queue).
+__host__ __device__ inline uint32_t entry_check(uint32_t fp_lo, uint32_t fp_hi, const int32_t* f) {
+  uint32_t h = fp_lo ^ (fp_hi * 0x9E3779B1u);
+  for (int i = 0; i < kEntFields; ++i) h = (h ^ uint32_t(f[i])) * 0x01000193u;
+  return h ^ (h >> 15);
+}
+
+// 64-bit fingerprint of a batch description as a plan is built for it.
+uint64_t batch_fingerprint(const int32_t* cu_suffix_host, const int32_t* prefix_len_host, int32_t batch,
+                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t num_splits);
 
 // Validates the ragged batch description shared by the device entry points.
 // Checks cu[0] == 0, cu non-decreasing, P_r >= 0 and a multiple of
@@ -33,5 +70,13 @@ cw_status check_batch(const int32_t* cu_suffix_host, const int32_t* prefix_len_h
 // Number of (request, kv head, row run) tiles of a batch, before padding.
 int64_t count_tiles(const int32_t* cu_suffix_host, int32_t batch, int32_t num_kv_heads,
                     int32_t positions_per_tile);
+
+// Checks a plan's header (plan_host, as cw_suffix_prefill_plan wrote it)
+// against the batch description of a device call: magic, fingerprint of
+// cu / prefix_len / heads / head_dim / split count, queue geometry. Sets the
+// launch grid, the split count, the fingerprint words and the entry count.
+cw_status check_plan_header(const char* what, const int32_t* plan_host, const int32_t* cu, const int32_t* plen,
+                            int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t* grid, int32_t* splits,
+                            uint32_t* fp_lo, uint32_t* fp_hi, int32_t* num_entries);
 
 }  // namespace cw

@@ -164,40 +164,53 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 // ---------------------------------------------------------------------------
 // Suffix prefill attention.
 //
-// Work split: one workgroup = 8 wavefronts (two per SIMD) = one tile of 256
-// packed query rows; wave w owns query columns 32 w .. 32 w + 31 and walks the
-// tile's keys in steps of 64.
+// Work: the host plan lists entries (request r, KV head g, a run of T suffix
+// rows, a run of 64-key steps); 256 packed MFMA rows of an entry hold the
+// G = Hq / Hkv query heads of g over T = 256 / G positions, so each K/V byte
+// staged in LDS serves the whole group. The grid is persistent: workgroup w
+// (8 wavefronts, two per SIMD) runs plan entries w, w + grid, w + 2 grid, ...
+// until an entry with r < 0, so one workgroup per CU walks its whole queue.
+//
+// Staging. LDS holds a ring of four stages of one 64-key step each (K and V^T
+// of 4 blocks). A copy cursor, independent of the entry being computed, walks
+// the workgroup's queue three steps ahead of the computation and copies each
+// step's blocks into ring position p % 4 with load-to-LDS instructions (no
+// registers): wave w moves K (w even) or V (w odd) of block w / 2 of the step.
+// Because the cursor crosses entry boundaries, the first steps of the next
+// entry are already in LDS while the current entry ends. A block that is not
+// whole (the prompt's partial last block) goes through registers and is
+// zero-filled past the prompt end; a missing block (past the prompt, or an
+// out-of-pool table entry) reads as zeros.
 //
 // Per wave the step loop is software-pipelined so that matrix and vector work
-// of different steps overlap inside one instruction stream:
-//   step j:  S(j+1) = K(j+1) Q^T  (16 MFMAs)  ||  P(j) = exp2(S(j))  (VALU)
-//            O^T += V(j)^T P(j)^T (16 MFMAs)  ||  mask + row max of S(j+1)
+// of different steps overlap in one instruction stream:
+//   step j:  S(j+1) = K(j+1) Q^T  (MFMA)  ||  P(j) = exp2(S(j)), row sums (VALU)
+//            O^T += V(j)^T P(j)^T (MFMA)  ||  mask + row max of S(j+1)      (VALU)
+// with the LDS operand reads of both products issued three MFMAs ahead.
 //
-// K/V staging: LDS holds three stages of (K, V) for one 64-key step. The
-// cache blocks are copied into LDS by the LDS-direct loads (global_load_lds),
-// which need no registers: wave w moves K (w even) or V (w odd) of block w / 2
-// of a step, K three steps and V two steps ahead of their use, and waits for
-// its copies of the step after next only at the end of the following step, so
-// each copy has two steps to land. A block that is missing or reaches past the
-// prompt end goes through registers instead and is zero-filled, so stale cache
-// bytes never meet a zero probability. One barrier ends each step.
+// Each wave owns 32 packed rows (query columns) and computes S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16: in the 32x32 accumulator a lane then holds one
+// query column and 16 keys, so the softmax state is lane-local and a row
+// reduction needs one exchange with lane ^ 32 (v_permlane32_swap). O^T = V^T
+// P^T uses the packed probabilities as the B operand; the cache keeps each V
+// block transposed, so V operands are plain 16-byte reads.
 //
 // Softmax in base 2 with lazy rescaling. Q is pre-multiplied by
 // softmax_scale * log2(e) (rounded to bf16), and each S accumulator starts
 // from -m, the running exponent base, so the MFMA result is already the
 // exponent s - m. The base moves only when a row's step maximum exceeds it by
-// more than 8 (a factor 256), and then O and l are rescaled once; probabilities
-// therefore stay below 256 and the fp32 sums cannot overflow.
+// more than 8 (a factor 256), and then O and l are rescaled once;
+// probabilities therefore stay below 256 and the fp32 sums cannot overflow.
 //
-// LDS layouts (per stage). A load-to-LDS instruction writes 64 x 16 bytes
-// contiguously in lane order, so swizzles are applied on the global side
-// (each lane fetches the 16 bytes that belong at its LDS slot).
-//  * K: row-major [key][d] (RB bytes per row); 16-byte chunk c of row r is
-//    stored at c ^ kswz(r), which puts the 16 rows of every operand read phase
-//    on distinct banks.
-//  * V: the cache holds each block transposed, [d][slot]; LDS keeps that per
-//    block ([block][d][16 keys], 32-byte rows) with the two 16-byte halves of
-//    row d swapped when bit 3 of d is set (conflict-free operand reads).
+// LDS layouts. A load-to-LDS instruction writes 64 x 16 bytes contiguously in
+// lane order, so swizzles are applied on the global side (each lane fetches
+// the 16 bytes that belong at its LDS slot).
+//  * K stages: row-major [key][d] (RB bytes per row); 16-byte chunk c of row r
+//    is stored at c ^ kswz(r), which puts the 16 rows of every operand read
+//    phase on distinct banks.
+//  * V stages (after the four K stages): each block as in the cache,
+//    [block][d][16 keys], 32-byte rows with the two 16-byte halves of row d
+//    swapped when bit 3 of d is set (conflict-free operand reads).
 //  * Key order: the PV MFMA's B operand is the score accumulator itself. In
 //    the 32x32 accumulator, lane half u, register e holds row
 //    8 (e / 4) + 4 u + e % 4. Reading K row pi(i) into A row i, with pi
@@ -207,15 +220,14 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 //    order: block kk, half u of a V^T row, one 16-byte read.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(4))) int32_t cint32_t;
 
 // The attention kernel orders its cache copies against its LDS reads itself,
-// with explicit vmcnt waits and workgroup barriers. Its two memory helpers are
-// asm statements so that the compiler does not add waits of its own: a
+// with explicit vmcnt waits and workgroup barriers. Its memory helpers are asm
+// statements so that the compiler does not add waits of its own: a
 // load-to-LDS copy it can see makes it put a vmcnt(0) before LDS reads it
-// cannot tell apart from the copy's target, and a register load it can see may
-// be waited for with vmcnt(0) far from its use. Either drains every copy in
-// flight. The compiler's own vmcnt waits only become more conservative for
-// memory operations it does not see.
+// cannot tell apart from the copy's target. The compiler's own vmcnt waits
+// only become more conservative for memory operations it does not see.
 
 // 16 bytes through registers, waited for at once (every older memory operation
 // of the wave completes with it). Used only for blocks that are not whole.
@@ -225,17 +237,26 @@ __device__ __forceinline__ u32x4 load16_now(const void* src) {
   return v;
 }
 
-// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l. M0 holds
-// the LDS address (one wait state between writing M0 and the copy).
-__device__ __forceinline__ void copy16_to_lds(const void* src, lds_void_t* dst) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(dst))) : "memory");
+// One load-to-LDS copy: lane l's 16 bytes at base + off land at lds + 16 l.
+// base is wave-uniform (SGPRs), off a per-lane 32-bit offset; M0 holds the LDS
+// address (one wait state between writing M0 and the copy).
+// (The uniform operands go through readfirstlane: the values are wave-uniform,
+// and this keeps them in SGPRs where the compiler cannot prove it.)
+__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t off, uint32_t lds_addr) {
+  const uint64_t b = reinterpret_cast<uintptr_t>(base);
+  // readfirstlane returns int: widen through uint32_t so the low half is not
+  // sign-extended into the high half
+  const uint64_t bu = (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b >> 32)))) << 32) |
+                      uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b))));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(bu), "s"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
 }
 
 constexpr int kAttnWaves = 8;
 constexpr int kAttnThreads = 64 * kAttnWaves;
 static_assert(kAttnWaves * 32 == cw::kTileRows, "one 32-column MFMA block per wave");
-constexpr int kStages = 3;
+constexpr int kStages = 4;   // LDS ring positions
+constexpr int kAhead = 3;    // the cursor copies a step this many steps before its use
 
 template <int D>
 struct AttnGeom {
@@ -244,13 +265,17 @@ struct AttnGeom {
   static constexpr int KTILE = kKv * RB;        // K of one step
   static constexpr int BLK = D * 2 * kBs;       // one V^T block (D rows of 16 keys)
   static constexpr int VTILE = (kKv / kBs) * BLK;
-  static constexpr int STAGE = KTILE + VTILE;
+  static constexpr int KREG = kStages * KTILE;  // the V stages start here
+  static constexpr int LDS = KREG + kStages * VTILE;
   static constexpr int RPL = 1024 / RB;         // K rows per 1 KB copy
   static constexpr int LPW = kBs * RB / 1024;   // 1 KB copies per block and tensor
   static constexpr int KS = D / 16;             // MFMA k-steps over D
   static constexpr int DT = D / 32;             // 32-row output tiles over D
   // chunk swizzle of K row r (rows of 256 bytes: 16 chunks; of 128 bytes: 8)
   __device__ static int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+  static_assert((kStages - 1) * KTILE + 32 * RB < 65536, "K read offsets are immediates");
+  static_assert((kStages - 1) * VTILE + 3 * BLK + (DT - 1) * 1024 < 65536, "V read offsets are immediates");
 };
 
 constexpr float kLazy = 8.0f;   // rescale when a score exceeds the base by 2^8
@@ -267,50 +292,56 @@ __device__ __forceinline__ bf16x8 scale_bf16x8(u32x4 raw, float c) {
   return __builtin_bit_cast(bf16x8, u32x4{o[0], o[1], o[2], o[3]});
 }
 
-// SPLIT: the key range of each tile is divided into num_splits runs of whole
-// steps processed by separate workgroups (workgroup s * num_tiles + i takes run s
-// of plan entry i); each writes, for its rows, the attention over its keys only:
-// O normalised in fp32 to part_o[s][row][d] and the base-2 log-sum-exp of the
-// scaled scores to part_lse[s][row] (row = suffix row * Hq + head), -inf when
-// no key of the run is visible. lse_merge_kernel combines the runs.
+// max(x of this lane, x of lane ^ 32)
+__device__ __forceinline__ float max_pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Plan layout shared with the host planner (words of int32).
+constexpr int kPlanHeader = cw::kPlanHeaderWords;
+constexpr int kEntryWords = cw::kPlanEntryWords;
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  const int32_t* bt;
+  const int32_t* plan;   // device copy of the whole plan (header, then entries)
+  uint16_t* out;
+  float* part_o;         // split runs: normalised O per run, fp32
+  float* part_lse;       // split runs: base-2 log-sum-exp per run
+  int64_t part_rows;     // rows of one run's part: total_s * Hq
+  int32_t bt_stride, hq, hkv, group, per_tile, num_blocks, num_entries;
+  float c_log2;
+  uint32_t fp_lo, fp_hi; // the batch fingerprint the host validated
+};
+
+// SPLIT: entries may cover only part of a tile's key range (the planner cuts
+// each tile into num_splits runs of whole steps); an entry then writes, for its
+// rows, the attention over its keys only: O normalised in fp32 to
+// part_o[split][row][d] and the base-2 log-sum-exp of the scaled scores to
+// part_lse[split][row] (row = suffix row * Hq + head), -inf when no key of the
+// run is visible. lse_merge_kernel combines the runs.
 template <int D, bool SPLIT>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-                                const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
-                                int bt_stride, const int32_t* __restrict__ cu,
-                                const int32_t* __restrict__ plen, const int4* __restrict__ plan,
-                                int batch, int hq, int hkv, int group, int per_tile, int num_blocks,
-                                float c_log2, uint16_t* __restrict__ out, int num_splits, int num_tiles,
-                                int64_t part_rows, float* __restrict__ part_o, float* __restrict__ part_lse) {
+void suffix_prefill_attn_kernel(const AttnArgs a) {
   using G = AttnGeom<D>;
   constexpr int KS = G::KS, DT = G::DT, RB = G::RB, NC = G::NC, LPW = G::LPW, RPL = G::RPL;
-  constexpr int KTILE = G::KTILE, BLK = G::BLK, STAGE = G::STAGE;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE];
+  constexpr int KTILE = G::KTILE, BLK = G::BLK, VTILE = G::VTILE, KREG = G::KREG;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[G::LDS];
+  const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
 
-  const int tile = SPLIT ? int(blockIdx.x % unsigned(num_tiles)) : int(blockIdx.x);
-  const int split = SPLIT ? int(blockIdx.x / unsigned(num_tiles)) : 0;
-  const int4 item = plan[tile];
-  const int r = item.x, g = item.y, row0 = item.z;
-  if (r < 0 || r >= batch || g < 0 || g >= hkv) return;
-  const int cu0 = cu[r];
-  const int S = cu[r + 1] - cu0;
-  const int P = plen[r];
-  if (row0 < 0 || row0 >= S) return;
-  const int L = P + S;
-  const int nvalid = min(per_tile, S - row0);
-  const int kv_end = P + row0 + nvalid;
-  const int ntiles = (kv_end + kKv - 1) / kKv;
-  // this workgroup's steps: tbeg .. tbeg + nsteps - 1 of the tile's key range
-  int tbeg = 0, nsteps = ntiles;
-  if (SPLIT) {
-    const int per = (ntiles + num_splits - 1) / num_splits;
-    tbeg = split * per;
-    nsteps = max(0, min(ntiles, tbeg + per) - tbeg);
-  }
-  // local steps 0 .. n_full - 1 are visible to every row of the tile (no mask)
-  const int n_full = max(0, min(nsteps, (P + row0 + 1) / kKv - tbeg));
-  const int nblk = (L + kBs - 1) / kBs;
-  const int32_t* btr = bt + int64_t(r) * bt_stride;
+  cint32_t* plan = reinterpret_cast<cint32_t*>(reinterpret_cast<uintptr_t>(a.plan));
+  // A plan whose header does not carry the fingerprint of the batch the host
+  // validated is not this batch's plan: compute nothing.
+  if (uint32_t(plan[2]) != a.fp_lo || uint32_t(plan[3]) != a.fp_hi) return;
+  cint32_t* ents = plan + kPlanHeader;
+  const int grid = int(gridDim.x);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -318,47 +349,13 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
   const int half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // This lane's query column.
-  const int m = wave * 32 + l32;
-  const int hh = m / per_tile;
-  const int pos = m - hh * per_tile;
-  const bool row_ok = (hh < group) && (pos < nvalid);
-  const int qpos = P + row0 + pos;  // keys 0 .. qpos are visible
-  const int64_t qrow = int64_t(cu0) + row0 + pos;
-  const int head = g * group + hh;
-
-  if (SPLIT && nsteps == 0) {   // no key of this run: an empty part
-    if (row_ok) {
-      const int64_t prow = int64_t(split) * part_rows + qrow * hq + head;
-      float* po = part_o + prow * D;
-#pragma unroll
-      for (int t = 0; t < DT; ++t)
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq)
-          *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (half == 0) part_lse[prow] = -INFINITY;
-    }
-    return;
-  }
-
-  bf16x8 qf[KS];
-  if (row_ok) {
-    const u32x4* qp = reinterpret_cast<const u32x4*>(q + (qrow * hq + head) * D);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s] = scale_bf16x8(qp[2 * s + half], c_log2);
-  } else {
-#pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
-  }
-
   // ---- staging role of this wave: tensor (K or V) of block slot bs of a step
   const int bs = wave >> 1;
   const bool is_v = (wave & 1) != 0;
-  const int ahead = is_v ? 2 : 3;   // step j copies the step j + ahead
-  const uint16_t* const cache = is_v ? vc : kc;
-  // Per-lane source offset inside a block (bytes) and LDS destination inside a
-  // stage of copy i (the destination of lane l is dst + 16 l).
-  int src_off[LPW];
+  const uint8_t* const cache = reinterpret_cast<const uint8_t*>(is_v ? a.vc : a.kc);
+  // Per-lane source offset inside a block and LDS destination of copy i
+  // (relative to the wave's block slot in a stage; lane l lands at +16 l).
+  uint32_t src_off[LPW];
 #pragma unroll
   for (int i = 0; i < LPW; ++i) {
     if (is_v) {
@@ -369,50 +366,80 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
       src_off[i] = row * RB + (((lane % NC) ^ G::kswz(row)) << 4);
     }
   }
-  const int dst0 = is_v ? KTILE + bs * BLK : bs * kBs * RB;
-  // Physical block of logical block lb, or -1 past the prompt / outside the
-  // pool; the table index is clamped into the request's row (always in bounds).
-  auto block_id = [&](int lb) __attribute__((always_inline)) -> int {
-    // read through the constant address space: a scalar load (a vector load
-    // would be waited for with vmcnt, which also waits for the copies)
-    const int b = reinterpret_cast<const __attribute__((address_space(4))) int32_t*>(
-        reinterpret_cast<uintptr_t>(btr))[min(lb, nblk - 1)];
-    return (lb < nblk && b >= 0 && b < num_blocks) ? b : -1;
-  };
-  // Stages step t's block of this wave into stage st; returns whether it used
-  // the load-to-LDS path (whose completion the caller then waits for).
-  auto stage_block = [&](int t, int b, int st) __attribute__((always_inline)) -> bool {
-    const int key0 = (tbeg + t) * kKv + bs * kBs;
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(cache) +
-                         (int64_t(b < 0 ? 0 : b) * hkv + g) * (kBs * RB);
-    uint8_t* dst = lds + st * STAGE + dst0;
-    if (b >= 0 && key0 + kBs <= L) {   // wave-uniform: the whole block is valid
+  const int slot0 = is_v ? KREG + bs * BLK : bs * kBs * RB;   // in stage 0
+  const int stage_stride = is_v ? VTILE : KTILE;
+
+  // ---- copy cursor: the entry and step whose blocks this wave copies next
+  int ce = blockIdx.x - grid;   // entry index
+  int cr = 0, cg = 0, cL = 0, ck = 0, cend = 0;
+  bool cdone = false;
+  auto cursor_next_entry = [&]() __attribute__((always_inline)) {
+    for (;;) {
+      ce += grid;
+      if (ce >= a.num_entries) { cdone = true; return; }
+      cint32_t* en = ents + int64_t(ce) * kEntryWords;
+      int32_t f[cw::kEntFields];
 #pragma unroll
-      for (int i = 0; i < LPW; ++i)
-        copy16_to_lds(src + src_off[i], (lds_void_t*)(dst + i * 1024));
-      return true;
+      for (int i = 0; i < cw::kEntFields; ++i) f[i] = en[i];
+      cr = f[cw::kEntR];
+      if (cr < 0 || uint32_t(en[cw::kEntCheck]) != cw::entry_check(a.fp_lo, a.fp_hi, f)) { cdone = true; return; }
+      cg = f[cw::kEntG];
+      cL = f[cw::kEntL];
+      ck = f[cw::kEntKbeg];
+      cend = f[cw::kEntKend];
+      if (ck < cend) return;
     }
-    const u32x4 zero{0, 0, 0, 0};
+  };
+  // Physical block of this wave's slot at the cursor's step, or -1 past the
+  // prompt / outside the pool; the table index is clamped into the row.
+  auto cursor_block = [&]() __attribute__((always_inline)) -> int {
+    const int nblk = (cL + kBs - 1) / kBs;
+    const int lb = ck * (kKv / kBs) + bs;
+    cint32_t* row = reinterpret_cast<cint32_t*>(reinterpret_cast<uintptr_t>(a.bt)) + int64_t(cr) * a.bt_stride;
+    const int b = row[min(lb, nblk - 1)];
+    return (lb < nblk && b >= 0 && b < a.num_blocks) ? b : -1;
+  };
+  cursor_next_entry();
+  int bnext = cdone ? -1 : cursor_block();
+  // Copies the cursor's step into ring position p and advances the cursor.
+  // Returns whether load-to-LDS copies of this wave are in flight (a block that
+  // is not whole is written through registers and waited for at once).
+  auto issue = [&](int p) __attribute__((always_inline)) -> bool {
+    if (cdone) return false;
+    const int b = bnext;
+    const int key0 = ck * kKv + bs * kBs;
+    const uint32_t dst = lds0 + (p & (kStages - 1)) * stage_stride + slot0;
+    const uint8_t* src = cache + (int64_t(b < 0 ? 0 : b) * a.hkv + cg) * (kBs * RB);
+    bool direct = false;
+    if (b >= 0 && key0 + kBs <= cL) {   // wave-uniform: the whole block is valid
 #pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-      u32x4 v = zero;
-      if (b >= 0) v = load16_now(src + src_off[i]);
-      if (is_v) {
-        // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
-        const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
-        const int vn = b < 0 ? 0 : min(8, max(0, L - key0 - h8));
+      for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
+      direct = true;
+    } else {
+      const u32x4 zero{0, 0, 0, 0};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
-      } else {
-        const bool ok = b >= 0 && key0 + RPL * i + lane / NC < L;
-        v = ok ? v : zero;
+      for (int i = 0; i < LPW; ++i) {
+        u32x4 v = zero;
+        if (b >= 0) v = load16_now(src + src_off[i]);
+        if (is_v) {
+          // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
+          const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
+          const int vn = b < 0 ? 0 : min(8, max(0, cL - key0 - h8));
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
+        } else {
+          const bool ok = b >= 0 && key0 + RPL * i + lane / NC < cL;
+          v = ok ? v : zero;
+        }
+        *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
       }
-      *reinterpret_cast<u32x4*>(dst + i * 1024 + lane * 16) = v;
     }
-    return false;
+    if (++ck == cend) cursor_next_entry();
+    bnext = cdone ? -1 : cursor_block();
+    return direct;
   };
-  // End of a step: this wave's copies for the next step have landed (the LPW
-  // copies issued in this step may still be in flight, when `keep` says that
+  // End of a step: this wave's copies for the next steps have landed (the
+  // copies issued in this step may still be in flight when `keep` says that
   // nothing else went to memory after them), LDS writes are done, then the
   // workgroup barrier. The empty asm statements keep the compiler from moving
   // memory accesses across the barrier.
@@ -424,203 +451,319 @@ void suffix_prefill_attn_kernel(const uint16_t* __restrict__ q, const uint16_t* 
     asm volatile("" ::: "memory");
   };
 
-  // ---- per-lane LDS read offsets (relative to a stage)
+  // ---- per-lane LDS read offsets (ring position 0; a position adds its stride)
   // K operand: row 32 h + pi(l32), logical chunk 2 s + half.
   const int k_row = (l32 & ~12) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
   int k_off[KS];
 #pragma unroll
   for (int s = 0; s < KS; ++s) k_off[s] = k_row * RB + (((2 * s + half) ^ G::kswz(k_row)) << 4);
   // V operand: block kk, row d = 32 t + l32, logical half = half.
-  const int v_off = KTILE + l32 * 32 + ((half ^ ((l32 >> 3) & 1)) << 4);
-
-  // ---- the four pieces of a step
-  // S^T = K Q^T for one stage, accumulators starting from c0.
-  auto qk = [&](const uint8_t* st, const f32x16& c0, f32x16 (&sc)[2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(st + k_off[s] + h * 32 * RB));
-        sc[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], s == 0 ? c0 : sc[h], 0, 0, 0);
-      }
-  };
-  // Causal mask of the step starting at key k0.
-  auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
-    // key of element e of half h is h 32 + (e / 8) 16 + half 8 + e % 8; the
-    // lane term moves to the limit so that the per-element terms stay immediates
-    const int lim = qpos - k0 - half * 8;
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        if (h * 32 + (e >> 3) * 16 + (e & 7) > lim) sc[h][e] = -INFINITY;
-  };
-  // Maximum of the row over the step's 64 keys (this lane's 32 and lane ^ 32's).
-  auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) -> float {
-    float a = fmaxf(fmaxf(sc[0][0], sc[0][1]), sc[0][2]);
-    float b = fmaxf(fmaxf(sc[1][0], sc[1][1]), sc[1][2]);
-#pragma unroll
-    for (int e = 3; e < 15; e += 2) {
-      a = fmaxf(fmaxf(a, sc[0][e]), sc[0][e + 1]);
-      b = fmaxf(fmaxf(b, sc[1][e]), sc[1][e + 1]);
-    }
-    a = fmaxf(fmaxf(a, sc[0][15]), sc[1][15]);
-    a = fmaxf(a, b);
-    return fmaxf(a, __shfl_xor(a, 32));
-  };
-  float l_run = 0.f;   // this lane's partial row sum (its 32 keys per step)
-  const bf16x2 ones{(__bf16)1.0f, (__bf16)1.0f};
-  // Probabilities 2^(s - m) as the PV B operand; adds their sum to l_run.
-  auto probs = [&](const f32x16 (&sc)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
-    float ls[2] = {0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int h = kk >> 1, e0 = (kk & 1) * 8;
-      uint32_t w[4];   // a scalar array: bit casts of ext-vector elements are not used
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        w[j] = pack_bf16x2(__builtin_amdgcn_exp2f(sc[h][e0 + 2 * j]),
-                           __builtin_amdgcn_exp2f(sc[h][e0 + 2 * j + 1]));
-        ls[kk & 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[j]), ones, ls[kk & 1], false);
-      }
-      pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-    }
-    l_run += ls[0] + ls[1];
-  };
-  f32x16 oacc[DT];
-#pragma unroll
-  for (int t = 0; t < DT; ++t) oacc[t] = f32x16{};
-  // O^T += V^T P^T for one stage.
-  auto pv = [&](const uint8_t* st, const bf16x8 (&pb)[4]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int t = 0; t < DT; ++t)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(st + v_off + kk * BLK + t * 1024));
-        oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], oacc[t], 0, 0, 0);
-      }
+  const int v_off = KREG + l32 * 32 + ((half ^ ((l32 >> 3) & 1)) << 4);
+  auto rd16 = [&](int addr) __attribute__((always_inline)) -> bf16x8 {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lds + addr));
   };
 
-  // ---- prologue: stage steps 0 and 1 (and K of step 2); S(0) with the exact
-  // row maximum as base
-  {
-    const int n0 = min(nsteps, ahead);
-    for (int t = 0; t < n0; ++t) stage_block(t, block_id((tbeg + t) * (kKv / kBs) + bs), t);
-  }
-  // block copied in step 0
-  int bnext = ahead < nsteps ? block_id((tbeg + ahead) * (kKv / kBs) + bs) : -1;
-  step_barrier(false);
-  f32x16 sa[2], sb[2];
-  qk(lds, f32x16{}, sa);
-  if (n_full == 0) mask(sa, tbeg * kKv);
-  f32x16 mneg;   // -m in every element: the start of each S accumulator
-  {
-    // Finite when the run's first step has a visible key for this row (always
-    // so for the first run: key 0 is visible to every row). A row that sees no
-    // key of the run's first step sees none of its later steps either (they
-    // hold higher keys), so any base serves it.
-    float m0 = rowmax(sa);
-    if (SPLIT && m0 == -INFINITY) m0 = 0.f;
+  // ---- first steps of the queue
+  int p = 0;   // ring position of the next step to compute
+  bool last_direct = false;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) sa[h] -= m0;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) mneg[e] = -m0;
-  }
-  float mx = 0.f;   // row maximum of the current S (relative to the base)
+  for (int i = 0; i < kAhead; ++i) last_direct = issue(i);
+  (void)last_direct;
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();   // K of stage 0 is refilled during step 0
+  __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 
-  // Moves the base up by the step maximum when it exceeds the base by kLazy.
-  auto rebase = [&](f32x16 (&sc)[2]) __attribute__((always_inline)) {
-    const bool grow = mx > kLazy;
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float delta = grow ? mx : 0.f;
-      const float alpha = __builtin_amdgcn_exp2f(-delta);
+  for (int e = blockIdx.x; e < a.num_entries; e += grid) {
+    cint32_t* en = ents + int64_t(e) * kEntryWords;
+    int32_t f[cw::kEntFields];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) sc[h] -= delta;
-      mneg -= delta;
-      l_run *= alpha;
-#pragma unroll
-      for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
-    }
-  };
-  // Step j < nsteps - 1: current S in sc, next S into sn. Stage of local step
-  // t is t % 3; this wave copies step j + ahead into stage (j + ahead) % 3.
-  auto step = [&](auto maskc, int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
-    constexpr bool MASK = decltype(maskc)::value;
-    rebase(sc);
-    const int tc = j + ahead;
-    bool issued = false;
-    if (tc < nsteps) issued = stage_block(tc, bnext, tc % kStages);
-    bnext = tc + 1 < nsteps ? block_id((tbeg + tc + 1) * (kKv / kBs) + bs) : -1;
-    bf16x8 pb[4];
-    qk(lds + ((j + 1) % kStages) * STAGE, mneg, sn);
-    probs(sc, pb);
-    pv(lds + (j % kStages) * STAGE, pb);
-    if (MASK) mask(sn, (tbeg + j + 1) * kKv);
-    mx = rowmax(sn);
-    // masked steps may spill registers to scratch memory: wait for everything
-    step_barrier(issued && !MASK);
-  };
-  using F = std::false_type;
-  using T = std::true_type;
-  const int last = nsteps - 1;
-  int j = 0;
-  // steps whose successor needs no mask, then the rest; two per iteration so
-  // the S buffers alternate without copies
-  auto run = [&](auto maskc, int end) __attribute__((always_inline)) {
-    for (; j + 1 < end; j += 2) {
-      step(maskc, j, sa, sb);
-      step(maskc, j + 1, sb, sa);
-    }
-    if (j < end) {
-      step(maskc, j, sa, sb);
-#pragma unroll
-      for (int h = 0; h < 2; ++h) sa[h] = sb[h];
-      ++j;
-    }
-  };
-  run(F{}, min(n_full - 1, last));
-  run(T{}, last);
-  {
-    rebase(sa);
-    bf16x8 pb[4];
-    probs(sa, pb);
-    pv(lds + (last % kStages) * STAGE, pb);
-  }
+    for (int i = 0; i < cw::kEntFields; ++i) f[i] = en[i];
+    // the end of the queue, or an entry that is not the one the planner wrote
+    if (f[cw::kEntR] < 0 || uint32_t(en[cw::kEntCheck]) != cw::entry_check(a.fp_lo, a.fp_hi, f)) break;
+    const int g = f[cw::kEntG], row0 = f[cw::kEntRow0], nvalid = f[cw::kEntNvalid];
+    const int cu0 = f[cw::kEntCu0], P = f[cw::kEntP];
+    const int kbeg = f[cw::kEntKbeg], kend = f[cw::kEntKend];
+    const int split = SPLIT ? f[cw::kEntSplit] : 0;
+    const int nsteps = kend - kbeg;
+    // local steps 0 .. n_full - 1 are visible to every row of the entry
+    const int n_full = max(0, min(nsteps, (P + row0 + 1) / kKv - kbeg));
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!row_ok) return;
-  if constexpr (SPLIT) {
-    const int64_t prow = int64_t(split) * part_rows + qrow * hq + head;
-    float* po = part_o + prow * D;
-    const bool any = l_tot > 0.f;
-    const float inv = any ? 1.f / l_tot : 0.f;
+    // This lane's query column.
+    const int m = wave * 32 + l32;
+    const int hh = m / a.per_tile;
+    const int pos = m - hh * a.per_tile;
+    const bool row_ok = (hh < a.group) && (pos < nvalid);
+    const int qpos = P + row0 + pos;  // keys 0 .. qpos are visible
+    const int64_t qrow = int64_t(cu0) + row0 + pos;
+    const int head = g * a.group + hh;
+
+    if (SPLIT && nsteps == 0) {   // no key of this run: an empty part
+      if (row_ok) {
+        const int64_t prow = int64_t(split) * a.part_rows + qrow * a.hq + head;
+        float* po = a.part_o + prow * D;
 #pragma unroll
-    for (int t = 0; t < DT; ++t)
+        for (int t = 0; t < DT; ++t)
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq)
-        *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) =
-            f32x4{oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv, oacc[t][gq * 4 + 2] * inv,
-                  oacc[t][gq * 4 + 3] * inv};
-    // base-2 log-sum-exp of the scaled scores: the base plus log2 of the sum
-    if (half == 0) part_lse[prow] = any ? -mneg[0] + __log2f(l_tot) : -INFINITY;
-    return;
-  }
-  const float inv = 1.f / l_tot;
-  uint16_t* op = out + (qrow * hq + head) * D;
-#pragma unroll
-  for (int t = 0; t < DT; ++t)
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int d = t * 32 + gq * 8 + half * 4;
-      const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
-                    pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
-      *reinterpret_cast<u32x2*>(op + d) = w;
+          for (int gq = 0; gq < 4; ++gq)
+            *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (half == 0) a.part_lse[prow] = -INFINITY;
+      }
+      continue;
     }
+
+    bf16x8 qf[KS];
+    if (row_ok) {
+      const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow * a.hq + head) * D);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qf[s] = scale_bf16x8(qp[2 * s + half], a.c_log2);
+    } else {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+    }
+
+    // Causal mask of the step starting at key k0.
+    auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
+      // key of element e of half h is h 32 + (e / 8) 16 + half 8 + e % 8; the
+      // lane term moves to the limit so that the per-element terms stay immediates
+      const int lim = qpos - k0 - half * 8;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e2 = 0; e2 < 16; ++e2)
+          if (h * 32 + (e2 >> 3) * 16 + (e2 & 7) > lim) sc[h][e2] = -INFINITY;
+    };
+    // Maximum of the row over a step's 64 keys (this lane's 32 and lane ^ 32's).
+    auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) -> float {
+      float x = fmaxf(fmaxf(sc[0][0], sc[0][1]), sc[0][2]);
+      float y = fmaxf(fmaxf(sc[1][0], sc[1][1]), sc[1][2]);
+#pragma unroll
+      for (int e2 = 3; e2 < 15; e2 += 2) {
+        x = fmaxf(fmaxf(x, sc[0][e2]), sc[0][e2 + 1]);
+        y = fmaxf(fmaxf(y, sc[1][e2]), sc[1][e2 + 1]);
+      }
+      x = fmaxf(fmaxf(x, sc[0][15]), sc[1][15]);
+      return max_pair32(fmaxf(x, y));
+    };
+
+    float l_run = 0.f;   // this lane's partial row sum (its 32 keys per step)
+    const bf16x2 ones{(__bf16)1.0f, (__bf16)1.0f};
+    f32x16 oacc[DT];
+#pragma unroll
+    for (int t = 0; t < DT; ++t) oacc[t] = f32x16{};
+    f32x16 mneg;   // -m in every element: the start of each S accumulator
+    float mx = 0.f;   // row maximum of the current S (relative to the base)
+
+    auto rdk = [&](int kb, int i) __attribute__((always_inline)) -> bf16x8 {   // K operand of QK MFMA i
+      return rd16(kb + k_off[i >> 1] + (i & 1) * 32 * RB);
+    };
+    auto rdv = [&](int vb, int i) __attribute__((always_inline)) -> bf16x8 {   // V operand of PV MFMA i
+      return rd16(vb + (i / DT) * BLK + (i % DT) * 1024);
+    };
+    // S^T = K Q^T over the K stage at `kb` (no other work), accumulators from zero.
+    auto qk_alone = [&](int kb, f32x16 (&sc)[2]) __attribute__((always_inline)) {
+      constexpr int N = 2 * KS;
+      bf16x8 kf[3];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, i);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        sc[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? f32x16{} : sc[i & 1], 0, 0, 0);
+        if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
+      }
+    };
+    // Probabilities of element pair i (of 16) of S: 2^(s - m) for two keys,
+    // packed to bf16, and their sum added to ls.
+    auto prob_pair = [&](const f32x16 (&sc)[2], int i, float& ls) __attribute__((always_inline)) -> uint32_t {
+      const int kk = i >> 2, jj = i & 3, h = kk >> 1, e = (kk & 1) * 8 + 2 * jj;
+      const uint32_t w = pack_bf16x2(__builtin_amdgcn_exp2f(sc[h][e]), __builtin_amdgcn_exp2f(sc[h][e + 1]));
+      ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, ls, false);
+      return w;
+    };
+    auto pack_pb = [&](const uint32_t (&w)[16], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk], w[4 * kk + 1], w[4 * kk + 2], w[4 * kk + 3]});
+    };
+    // Phase A of a step: S(j+1) = K Q^T from the stage at `kb`, accumulators
+    // from -m (sn), interleaved with the probabilities of S(j) (sc -> pb). Each
+    // group is one MFMA, the operand read three MFMAs ahead and one element
+    // pair of the softmax; the scheduling barriers keep that order.
+    auto phase_a = [&](int kb, const f32x16 (&sc)[2], f32x16 (&sn)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+      static_assert(2 * KS >= 16 || D == 64, "element pairs per MFMA");
+      constexpr int N = 2 * KS;
+      constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
+      uint32_t w[16];
+      float ls[2] = {0.f, 0.f};
+      bf16x8 kf[3];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, i);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? mneg : sn[i & 1], 0, 0, 0);
+        if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
+#pragma unroll
+        for (int u = 0; u < PER; ++u) w[i * PER + u] = prob_pair(sc, i * PER + u, ls[(i * PER + u) & 1]);
+      }
+      // scheduling pattern: three operand reads, then per MFMA: the MFMA, the
+      // read three ahead, softmax VALU
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i + 3 < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4 * PER + 1, 0);
+      }
+      pack_pb(w, pb);
+      l_run += ls[0] + ls[1];
+    };
+    // Probabilities of S alone (the last step of an entry).
+    auto probs_alone = [&](const f32x16 (&sc)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+      uint32_t w[16];
+      float ls[2] = {0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < 16; ++i) w[i] = prob_pair(sc, i, ls[i & 1]);
+      pack_pb(w, pb);
+      l_run += ls[0] + ls[1];
+    };
+    // Phase B of a step: O^T += V^T P^T from the stage at `vb`, interleaved
+    // with the row maximum of sn (when sn is given; already masked).
+    auto phase_b = [&](int vb, const bf16x8 (&pb)[4], const f32x16* sn) __attribute__((always_inline)) -> float {
+      constexpr int N = 4 * DT;
+      constexpr int PER = 16 / N;   // max3 operations per MFMA
+      float x[2] = {-INFINITY, -INFINITY};
+      bf16x8 vf[3];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, i);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pb[i / DT], oacc[i % DT], 0, 0, 0);
+        if (i + 3 < N) vf[i % 3] = rdv(vb, i + 3);
+        if (sn) {
+#pragma unroll
+          for (int u = 0; u < PER; ++u) {
+            const int q = i * PER + u, h = q & 1, e = (q >> 1) * 2;
+            x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i + 3 < N) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (sn) __builtin_amdgcn_sched_group_barrier(0x002, PER, 0);
+      }
+      return sn ? max_pair32(fmaxf(x[0], x[1])) : 0.f;
+    };
+    // Moves the base up by the step maximum when it exceeds the base by kLazy.
+    auto rebase = [&](f32x16 (&sc)[2]) __attribute__((always_inline)) {
+      const bool grow = mx > kLazy;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float delta = grow ? mx : 0.f;
+        const float alpha = __builtin_amdgcn_exp2f(-delta);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) sc[h] -= delta;
+        mneg -= delta;
+        l_run *= alpha;
+#pragma unroll
+        for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
+      }
+    };
+    auto kbase = [&](int pp) { return (pp & (kStages - 1)) * KTILE; };
+    auto vbase = [&](int pp) { return v_off + (pp & (kStages - 1)) * VTILE; };
+
+    // ---- S(0) with the exact row maximum as base
+    f32x16 sa[2], sb[2];
+    qk_alone(kbase(p), sa);
+    if (n_full == 0) mask(sa, kbeg * kKv);
+    {
+      // Finite when the run's first step has a visible key for this row (always
+      // so for the first run: key 0 is visible to every row). A row that sees no
+      // key of the run's first step sees none of its later steps either (they
+      // hold higher keys), so any base serves it.
+      float m0 = rowmax(sa);
+      if (m0 == -INFINITY) m0 = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) sa[h] -= m0;
+#pragma unroll
+      for (int e2 = 0; e2 < 16; ++e2) mneg[e2] = -m0;
+    }
+
+    // Step j < nsteps - 1 at ring position p: current S in sc, next S into sn;
+    // MASK: S(j+1) crosses the causal diagonal.
+    auto step = [&](auto maskc, int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
+      constexpr bool MASK = decltype(maskc)::value;
+      const bool direct = issue(p + kAhead);
+      rebase(sc);
+      bf16x8 pb[4];
+      phase_a(kbase(p + 1), sc, sn, pb);
+      if (MASK) mask(sn, (kbeg + j + 1) * kKv);
+      mx = phase_b(vbase(p), pb, sn);
+      step_barrier(direct);
+      ++p;
+    };
+    using F = std::false_type;
+    using T = std::true_type;
+    const int last = nsteps - 1;
+    int j = 0;
+    // steps whose successor needs no mask, then the rest; two per iteration so
+    // the S buffers alternate without copies
+    auto run = [&](auto maskc, int end) __attribute__((always_inline)) {
+      for (; j + 1 < end; j += 2) {
+        step(maskc, j, sa, sb);
+        step(maskc, j + 1, sb, sa);
+      }
+      if (j < end) {
+        step(maskc, j, sa, sb);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) sa[h] = sb[h];
+        ++j;
+      }
+    };
+    run(F{}, min(n_full - 1, last));
+    run(T{}, last);
+    {   // the entry's last step: P and PV only
+      const bool direct = issue(p + kAhead);
+      rebase(sa);
+      bf16x8 pb[4];
+      probs_alone(sa, pb);
+      phase_b(vbase(p), pb, nullptr);
+      step_barrier(direct);
+      ++p;
+    }
+
+    const float l_tot = sum_pair32(l_run);
+    if (!row_ok) continue;
+    if constexpr (SPLIT) {
+      const int64_t prow = int64_t(split) * a.part_rows + qrow * a.hq + head;
+      float* po = a.part_o + prow * D;
+      const bool any = l_tot > 0.f;
+      const float inv = any ? 1.f / l_tot : 0.f;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq)
+          *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) =
+              f32x4{oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv, oacc[t][gq * 4 + 2] * inv,
+                    oacc[t][gq * 4 + 3] * inv};
+      // base-2 log-sum-exp of the scaled scores: the base plus log2 of the sum
+      if (half == 0) a.part_lse[prow] = any ? -mneg[0] + __log2f(l_tot) : -INFINITY;
+    } else {
+      const float inv = 1.f / l_tot;
+      uint16_t* op = a.out + (qrow * a.hq + head) * D;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          const int d = t * 32 + gq * 8 + half * 4;
+          const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
+                        pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
+          *reinterpret_cast<u32x2*>(op + d) = w;
+        }
+    }
+  }
+  // Every copy the cursor issued was consumed: the cursor runs out with the
+  // last entry, and every issued step is computed before the loop ends.
 }
 
 // ---------------------------------------------------------------------------
@@ -701,9 +844,10 @@ extern "C" cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_
 
 namespace {
 
-// Checks shared by both attention entry points; fills the launch geometry.
-struct AttnShape {
-  int group = 0, per_tile = 0;
+// Checks shared by the attention entry points; fills the launch arguments.
+struct AttnLaunch {
+  AttnArgs args;
+  int32_t grid = 0, splits = 1;
   int64_t rows = 0;
 };
 cw_status check_attn(const char* what, const void* q, const void* k_cache, const void* v_cache,
@@ -711,8 +855,8 @@ cw_status check_attn(const char* what, const void* q, const void* k_cache, const
                      const int32_t* prefix_len_dev, const int32_t* cu_suffix_host,
                      const int32_t* prefix_len_host, int32_t batch, int32_t num_q_heads,
                      int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t num_blocks,
-                     float softmax_scale, const int32_t* plan_dev, int32_t num_tiles, const void* out,
-                     AttnShape* shape) {
+                     float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev, const void* out,
+                     AttnLaunch* L) {
   const std::string w(what);
   if (!q || !k_cache || !v_cache || !block_table || !cu_suffix_dev || !prefix_len_dev || !out)
     return cw::fail(CW_EINVAL, w + ": a required pointer is NULL");
@@ -723,46 +867,43 @@ cw_status check_attn(const char* what, const void* q, const void* k_cache, const
     return cw::fail(CW_EINVAL, w + ": softmax_scale must be finite and positive");
   if (head_dim != 64 && head_dim != 128) return cw::fail(CW_EUNSUPPORTED, w + ": head_dim must be 64 or 128");
   if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, w + ": block_size must be 16");
-  shape->group = num_q_heads / num_kv_heads;
-  if (shape->group > cw::kMaxGroup)
-    return cw::fail(CW_EUNSUPPORTED, w + ": more than 128 query heads per KV head");
-  cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &shape->rows);
+  const int group = num_q_heads / num_kv_heads;
+  if (group > cw::kMaxGroup) return cw::fail(CW_EUNSUPPORTED, w + ": more than 128 query heads per KV head");
+  cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &L->rows);
   if (st != CW_OK) return st;
-  shape->per_tile = cw::tile_positions(shape->group);
-  const int64_t need = cw::count_tiles(cu_suffix_host, batch, num_kv_heads, shape->per_tile);
-  if (num_tiles < need || int64_t(num_tiles) > need * cw::kNumXcd)
-    return cw::fail(CW_EINVAL, w + ": num_tiles " + std::to_string(num_tiles) + " does not match the batch (" +
-                                   std::to_string(need) + " tiles)");
-  if (num_tiles > 0 && !plan_dev) return cw::fail(CW_EINVAL, w + ": plan_dev is required");
+  AttnArgs& a = L->args;
+  st = cw::check_plan_header(what, plan_host, cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
+                             head_dim, &L->grid, &L->splits, &a.fp_lo, &a.fp_hi, &a.num_entries);
+  if (st != CW_OK) return st;
+  if (L->grid > 0 && !plan_dev) return cw::fail(CW_EINVAL, w + ": plan_dev is required");
+  a.q = static_cast<const uint16_t*>(q);
+  a.kc = static_cast<const uint16_t*>(k_cache);
+  a.vc = static_cast<const uint16_t*>(v_cache);
+  a.bt = block_table;
+  a.plan = plan_dev;
+  a.out = static_cast<uint16_t*>(const_cast<void*>(out));
+  a.part_o = nullptr;
+  a.part_lse = nullptr;
+  a.part_rows = L->rows * num_q_heads;
+  a.bt_stride = bt_stride;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.group = group;
+  a.per_tile = cw::tile_positions(group);
+  a.num_blocks = num_blocks;
+  a.c_log2 = softmax_scale * 1.4426950408889634f;
   return CW_OK;
 }
 
 template <bool SPLIT>
-void launch_attn(int head_dim, unsigned grid, hipStream_t s, const void* q, const void* k_cache,
-                 const void* v_cache, const int32_t* block_table, int32_t bt_stride,
-                 const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev, const int32_t* plan_dev,
-                 int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, const AttnShape& sh,
-                 int32_t num_blocks, float softmax_scale, void* out, int num_splits, int num_tiles,
-                 int64_t part_rows, float* part_o, float* part_lse) {
-  const float c_log2 = softmax_scale * 1.4426950408889634f;
-  auto* qp = static_cast<const uint16_t*>(q);
-  auto* kp = static_cast<const uint16_t*>(k_cache);
-  auto* vp = static_cast<const uint16_t*>(v_cache);
-  auto* pp = reinterpret_cast<const int4*>(plan_dev);
-  auto* op = static_cast<uint16_t*>(out);
+void launch_attn(int head_dim, const AttnLaunch& L, hipStream_t s) {
   if (head_dim == 128)
-    hipLaunchKernelGGL((suffix_prefill_attn_kernel<128, SPLIT>), dim3(grid), dim3(kAttnThreads), 0, s, qp, kp, vp,
-                       block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch, num_q_heads,
-                       num_kv_heads, sh.group, sh.per_tile, num_blocks, c_log2, op, num_splits, num_tiles,
-                       part_rows, part_o, part_lse);
+    hipLaunchKernelGGL((suffix_prefill_attn_kernel<128, SPLIT>), dim3(unsigned(L.grid)), dim3(kAttnThreads), 0, s,
+                       L.args);
   else
-    hipLaunchKernelGGL((suffix_prefill_attn_kernel<64, SPLIT>), dim3(grid), dim3(kAttnThreads), 0, s, qp, kp, vp,
-                       block_table, bt_stride, cu_suffix_dev, prefix_len_dev, pp, batch, num_q_heads,
-                       num_kv_heads, sh.group, sh.per_tile, num_blocks, c_log2, op, num_splits, num_tiles,
-                       part_rows, part_o, part_lse);
+    hipLaunchKernelGGL((suffix_prefill_attn_kernel<64, SPLIT>), dim3(unsigned(L.grid)), dim3(kAttnThreads), 0, s,
+                       L.args);
 }
-
-constexpr int kMaxSplits = 64;
 
 // Workspace of the split path: part_o [splits][rows][D] fp32, then part_lse
 // [splits][rows] fp32 at a 256-byte aligned offset.
@@ -789,24 +930,24 @@ extern "C" cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, 
                                             const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                             int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                             int32_t head_dim, int32_t block_size, int32_t num_blocks,
-                                            float softmax_scale, const int32_t* plan_dev,
-                                            int32_t num_tiles, void* out, void* stream) {
-  AttnShape sh;
+                                            float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev,
+                                            void* out, void* stream) {
+  AttnLaunch L;
   cw_status st = check_attn("suffix_prefill_attn", q, k_cache, v_cache, block_table, bt_stride, cu_suffix_dev,
                             prefix_len_dev, cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
-                            head_dim, block_size, num_blocks, softmax_scale, plan_dev, num_tiles, out, &sh);
+                            head_dim, block_size, num_blocks, softmax_scale, plan_host, plan_dev, out, &L);
   if (st != CW_OK) return st;
-  if (sh.rows == 0 || num_tiles == 0) return cw::ok();
-  launch_attn<false>(head_dim, unsigned(num_tiles), static_cast<hipStream_t>(stream), q, k_cache, v_cache,
-                     block_table, bt_stride, cu_suffix_dev, prefix_len_dev, plan_dev, batch, num_q_heads,
-                     num_kv_heads, sh, num_blocks, softmax_scale, out, 1, num_tiles, 0, nullptr, nullptr);
+  if (L.splits != 1)
+    return cw::fail(CW_EINVAL, "suffix_prefill_attn: the plan has splits; use cw_suffix_prefill_attn_split");
+  if (L.rows == 0 || L.grid == 0) return cw::ok();
+  launch_attn<false>(head_dim, L, static_cast<hipStream_t>(stream));
   return check_launch("suffix_prefill_attn launch");
 }
 
 extern "C" int64_t cw_suffix_prefill_split_workspace_bytes(int64_t total_rows, int32_t num_q_heads,
                                                            int32_t head_dim, int32_t num_splits) {
   if (total_rows < 0 || num_q_heads < 1 || (head_dim != 64 && head_dim != 128) || num_splits < 1 ||
-      num_splits > kMaxSplits)
+      num_splits > cw::kMaxSplits)
     return cw::fail(CW_EINVAL, "suffix_prefill_split_workspace_bytes: invalid argument");
   const int64_t part_rows = total_rows * num_q_heads;
   return split_lse_offset(part_rows, head_dim, num_splits) + int64_t(num_splits) * part_rows * 4;
@@ -818,34 +959,27 @@ extern "C" cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_c
                                                   const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                                   int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                                   int32_t head_dim, int32_t block_size, int32_t num_blocks,
-                                                  float softmax_scale, const int32_t* plan_dev,
-                                                  int32_t num_tiles, int32_t num_splits, void* workspace,
-                                                  int64_t workspace_bytes, void* out, void* stream) {
-  AttnShape sh;
+                                                  float softmax_scale, const int32_t* plan_host,
+                                                  const int32_t* plan_dev, void* workspace, int64_t workspace_bytes,
+                                                  void* out, void* stream) {
+  AttnLaunch L;
   cw_status st = check_attn("suffix_prefill_attn_split", q, k_cache, v_cache, block_table, bt_stride,
                             cu_suffix_dev, prefix_len_dev, cu_suffix_host, prefix_len_host, batch, num_q_heads,
-                            num_kv_heads, head_dim, block_size, num_blocks, softmax_scale, plan_dev, num_tiles,
-                            out, &sh);
+                            num_kv_heads, head_dim, block_size, num_blocks, softmax_scale, plan_host, plan_dev,
+                            out, &L);
   if (st != CW_OK) return st;
-  if (num_splits < 1 || num_splits > kMaxSplits)
-    return cw::fail(CW_EINVAL, "suffix_prefill_attn_split: num_splits must be in [1, 64]");
-  if (int64_t(num_tiles) * num_splits > INT32_MAX)
-    return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_attn_split: too many workgroups");
-  const int64_t part_rows = sh.rows * num_q_heads;
-  const int64_t need = cw_suffix_prefill_split_workspace_bytes(sh.rows, num_q_heads, head_dim, num_splits);
+  const int64_t need = cw_suffix_prefill_split_workspace_bytes(L.rows, num_q_heads, head_dim, L.splits);
   if (!workspace || workspace_bytes < need)
     return cw::fail(CW_EINVAL, "suffix_prefill_attn_split: workspace must hold " + std::to_string(need) + " bytes");
-  if (sh.rows == 0 || num_tiles == 0) return cw::ok();
+  if (L.rows == 0 || L.grid == 0) return cw::ok();
   auto* s = static_cast<hipStream_t>(stream);
-  auto* part_o = static_cast<float*>(workspace);
-  auto* part_lse = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
-                                            split_lse_offset(part_rows, head_dim, num_splits));
-  launch_attn<true>(head_dim, unsigned(int64_t(num_tiles) * num_splits), s, q, k_cache, v_cache, block_table,
-                    bt_stride, cu_suffix_dev, prefix_len_dev, plan_dev, batch, num_q_heads, num_kv_heads, sh,
-                    num_blocks, softmax_scale, out, num_splits, num_tiles, part_rows, part_o, part_lse);
+  L.args.part_o = static_cast<float*>(workspace);
+  L.args.part_lse = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
+                                             split_lse_offset(L.args.part_rows, head_dim, L.splits));
+  launch_attn<true>(head_dim, L, s);
   st = check_launch("suffix_prefill_attn_split launch");
   if (st != CW_OK) return st;
-  return launch_merge(part_o, part_lse, num_splits, part_rows, head_dim, out, s);
+  return launch_merge(L.args.part_o, L.args.part_lse, L.splits, L.args.part_rows, head_dim, out, s);
 }
 
 extern "C" cw_status cw_lse_merge(const void* partial_o, const void* partial_lse, int32_t num_parts,

@@ -26,6 +26,10 @@ CW_ENOSPC = -3
 CW_EHIP = -4
 BLOCK_SIZE = 16
 TILE_ROWS = 256    # packed query rows (heads x positions) of one attention tile (cw.h)
+PLAN_HEADER = 16   # int32 words of a plan's header, then entries of PLAN_ENTRY words
+PLAN_ENTRY = 16
+HDR_ENTRIES, HDR_GRID, HDR_SPLITS, HDR_QUEUE_LEN, HDR_WORK = 1, 4, 5, 11, 12
+ENT_R, ENT_G, ENT_ROW0, ENT_NVALID, ENT_CU0, ENT_P, ENT_L, ENT_KBEG, ENT_KEND, ENT_SPLIT = range(10)
 
 _i32 = ctypes.c_int32
 _i64 = ctypes.c_int64
@@ -64,15 +68,15 @@ def _load() -> ctypes.CDLL:
         "cw_release_batch": (_i32, [_vp, _pi32, _i32, _pi32, _pi32, _i32, _i32]),
         "cw_kv_append": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
                                 _i32, _i32, _i32, _i32, _i32, _vp]),
-        "cw_suffix_prefill_plan_words": (_i64, [_pi32, _pi32, _i32, _i32, _i32, _i32]),
-        "cw_suffix_prefill_plan": (_i32, [_pi32, _pi32, _i32, _i32, _i32, _i32, _pi32, _i64, _pi32]),
+        "cw_suffix_prefill_plan_words": (_i64, [_pi32, _pi32, _i32, _i32, _i32, _i32, _i32]),
+        "cw_suffix_prefill_plan": (_i32, [_pi32, _pi32, _i32, _i32, _i32, _i32, _i32, _pi32, _i64]),
         "cw_suffix_prefill_attn": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
-                                          _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _i32,
+                                          _i32, _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp,
                                           _vp, _vp]),
         "cw_suffix_prefill_split_workspace_bytes": (_i64, [_i64, _i32, _i32, _i32]),
         "cw_suffix_prefill_attn_split": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
-                                                _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _i32,
-                                                _i32, _vp, _i64, _vp, _vp]),
+                                                _i32, _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp,
+                                                _vp, _i64, _vp, _vp]),
         "cw_lse_merge": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp, _vp]),
         "cw_tree_create": (_i32, [_i32, ctypes.POINTER(_vp)]),
         "cw_tree_destroy": (None, [_vp]),
@@ -295,21 +299,27 @@ def release_batch(pool: Pool, block_table, prefix_len, cu_suffix, block_size: in
                                  _ptr(cu, ctypes.c_int32), len(plen), block_size))
 
 
-def suffix_prefill_plan(cu_suffix, prefix_len, num_q_heads: int, num_kv_heads: int, head_dim: int):
-    """cw_suffix_prefill_plan: returns (plan int32 array, num_tiles)."""
+def suffix_prefill_plan(cu_suffix, prefix_len, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                        num_splits: int = 1) -> np.ndarray:
+    """cw_suffix_prefill_plan: the plan (int32 array: header, then entries)."""
     cu = _i32_array(cu_suffix, "cu_suffix")
     plen = _i32_array(prefix_len, "prefix_len")
     B = len(plen)
     words = int(_lib.cw_suffix_prefill_plan_words(_ptr(cu, ctypes.c_int32), _ptr(plen, ctypes.c_int32), B,
-                                                  num_q_heads, num_kv_heads, head_dim))
+                                                  num_q_heads, num_kv_heads, head_dim, int(num_splits)))
     if words < 0:
         _check(words)
-    plan = np.zeros(max(words, 4), dtype=np.int32)
-    n = ctypes.c_int32(0)
+    plan = np.zeros(words, dtype=np.int32)
     _check(_lib.cw_suffix_prefill_plan(_ptr(cu, ctypes.c_int32), _ptr(plen, ctypes.c_int32), B, num_q_heads,
-                                       num_kv_heads, head_dim, _ptr(plan, ctypes.c_int32), len(plan),
-                                       ctypes.byref(n)))
-    return plan[:4 * n.value].copy(), n.value
+                                       num_kv_heads, head_dim, int(num_splits), _ptr(plan, ctypes.c_int32),
+                                       len(plan)))
+    return plan
+
+
+def plan_entries(plan: np.ndarray) -> np.ndarray:
+    """The entries of a plan as an [n, PLAN_ENTRY] view (padding included:
+    entries with request -1 end a queue)."""
+    return plan[PLAN_HEADER:].reshape(-1, PLAN_ENTRY)
 
 
 # ---------------------------------------------------------------- device calls
@@ -334,6 +344,8 @@ def _stream(stream) -> int:
 # Debug mode: every device call first checks that the device copies of the
 # batch description (block table, offsets, prefix lengths, plan) equal the host
 # copies that validated it. The check synchronises the device; off by default.
+# (Without it the library still refuses a host plan built for another batch,
+# and the kernels compute nothing for a device plan whose header differs.)
 DEBUG_CHECK_COPIES = os.environ.get("CW_DEBUG_CHECK_COPIES", "") not in ("", "0")
 
 
@@ -354,7 +366,8 @@ class BatchMeta:
     """Host and device copies of a ragged batch's description.
 
     block_table [B, stride], cu_suffix [B + 1], prefix_len [B] (int32); the
-    plan is built on the host by the library. With device=None nothing is
+    attention plan is built on the host by the library (plans for split counts
+    other than 1 are built on first use and kept). With device=None nothing is
     uploaded and the caller assigns the device tensors bt, cu, plen, plan."""
 
     def __init__(self, block_table, cu_suffix, prefix_len, num_q_heads: int, num_kv_heads: int,
@@ -368,16 +381,15 @@ class BatchMeta:
             raise ValueError("cu_suffix must have batch + 1 entries")
         self.batch = len(self.plen_host)
         self.num_q_heads, self.num_kv_heads, self.head_dim = num_q_heads, num_kv_heads, head_dim
-        self.plan_host, self.num_tiles = suffix_prefill_plan(self.cu_host, self.plen_host, num_q_heads,
-                                                             num_kv_heads, head_dim)
+        self.plan_host = suffix_prefill_plan(self.cu_host, self.plen_host, num_q_heads, num_kv_heads, head_dim)
         self.device = device
         self.bt = self.cu = self.plen = self.plan = None
+        self._split_plans = {}
         if device is not None:
             self.bt = torch.from_numpy(self.bt_host).to(device)
             self.cu = torch.from_numpy(self.cu_host).to(device)
             self.plen = torch.from_numpy(self.plen_host).to(device)
-            plan = self.plan_host if self.plan_host.size else np.zeros(4, np.int32)
-            self.plan = torch.from_numpy(plan).to(device)
+            self.plan = torch.from_numpy(self.plan_host).to(device)
 
     @property
     def total_rows(self) -> int:
@@ -387,6 +399,22 @@ class BatchMeta:
     def bt_stride(self) -> int:
         return int(self.bt_host.shape[1])
 
+    @property
+    def num_tiles(self) -> int:
+        """Tiles of the batch (plan entries of the unsplit plan, padding excluded)."""
+        return int((plan_entries(self.plan_host)[:, ENT_R] >= 0).sum())
+
+    def split_plan(self, num_splits: int):
+        """(host plan, device plan) for `num_splits` key runs per tile."""
+        if num_splits == 1:
+            return self.plan_host, self.plan
+        if num_splits not in self._split_plans:
+            ph = suffix_prefill_plan(self.cu_host, self.plen_host, self.num_q_heads, self.num_kv_heads,
+                                     self.head_dim, num_splits)
+            pd = torch.from_numpy(ph).to(self.device) if self.device is not None else None
+            self._split_plans[num_splits] = (ph, pd)
+        return self._split_plans[num_splits]
+
     def _hp(self, a):
         return _ptr(a, ctypes.c_int32)
 
@@ -394,9 +422,11 @@ class BatchMeta:
         """The caller guarantees that the device copies equal the host ones
         (the library validates and plans with the host copies, the kernels
         read the device copies); this checks it, synchronising the device."""
-        plan = self.plan_host if self.plan_host.size else np.zeros(4, np.int32)
-        _check_copies((("block_table", self.bt, self.bt_host), ("cu_suffix", self.cu, self.cu_host),
-                       ("prefix_len", self.plen, self.plen_host), ("plan", self.plan, plan)))
+        pairs = [("block_table", self.bt, self.bt_host), ("cu_suffix", self.cu, self.cu_host),
+                 ("prefix_len", self.plen, self.plen_host), ("plan", self.plan, self.plan_host)]
+        for n, (ph, pd) in self._split_plans.items():
+            pairs.append((f"plan ({n} splits)", pd, ph))
+        _check_copies(pairs)
 
 
 def _cache_shapes_ok(k_cache: torch.Tensor, v_cache: torch.Tensor, hkv: int, D: int) -> bool:
@@ -481,15 +511,15 @@ def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
         _dev(v_cache, torch.bfloat16, "v_cache"), _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
         _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
         meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
-        k_cache.shape[0], float(softmax_scale), _dev(meta.plan, torch.int32, "plan"), meta.num_tiles,
+        k_cache.shape[0], float(softmax_scale), meta._hp(meta.plan_host), _dev(meta.plan, torch.int32, "plan"),
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
 
 def split_count(meta: BatchMeta, num_cus: int = 256) -> int:
     """A split count for cw_suffix_prefill_attn_split: enough runs that the
-    batch's tiles cover every CU once (one attention workgroup fits per CU)."""
-    return max(1, min(64, num_cus // max(1, meta.num_tiles)))
+    batch's tiles cover every CU at least once (one attention workgroup per CU)."""
+    return max(1, min(64, -(-num_cus // max(1, meta.num_tiles))))
 
 
 def split_workspace_bytes(meta: BatchMeta, num_splits: int) -> int:
@@ -521,13 +551,14 @@ def suffix_prefill_attn_split(meta: BatchMeta, q: torch.Tensor, k_cache: torch.T
     need = split_workspace_bytes(meta, num_splits)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    plan_host, plan_dev = meta.split_plan(int(num_splits))
     _check(_lib.cw_suffix_prefill_attn_split(
         _dev(q, torch.bfloat16, "q"), _dev(k_cache, torch.bfloat16, "k_cache"),
         _dev(v_cache, torch.bfloat16, "v_cache"), _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
         _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
         meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
-        k_cache.shape[0], float(softmax_scale), _dev(meta.plan, torch.int32, "plan"), meta.num_tiles,
-        int(num_splits), _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+        k_cache.shape[0], float(softmax_scale), meta._hp(plan_host), _dev(plan_dev, torch.int32, "plan"),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
@@ -576,10 +607,11 @@ class BatchRunner:
         max_cu[1:] = np.cumsum(np.diff(self.cu_tokens))
         zero = np.zeros(B, dtype=np.int32)
         words = int(_lib.cw_suffix_prefill_plan_words(_ptr(max_cu, ctypes.c_int32), _ptr(zero, ctypes.c_int32),
-                                                      B, num_q_heads, num_kv_heads, head_dim))
+                                                      B, num_q_heads, num_kv_heads, head_dim, 1))
         if words < 0:
             _check(words)
-        self.plan_capacity = max(words, 4) * 8
+        # queues of uneven entry counts pad to the longest: leave room for that
+        self.plan_capacity = max(2 * words, PLAN_HEADER + PLAN_ENTRY * 256 * 8)
         # One host buffer (pinned when a GPU is present) and one device buffer
         # hold [block table | cu_suffix | prefix_len | plan], so a step uploads
         # its schedule with a single asynchronous copy. Sections start on
@@ -597,14 +629,13 @@ class BatchRunner:
         self.plen_host = h[o_pl:o_pl + B]
         self.plan_host = h[o_plan:o_plan + self.plan_capacity]
         self._o_plan = o_plan
-        self.num_tiles = 0
+        self.plan_words = 0
         self.device = device
         self._dev = torch.empty(total, dtype=torch.int32, device=device)
         self.bt = self._dev[o_bt:o_bt + B * bt_stride].view(B, bt_stride)
         self.cu = self._dev[o_cu:o_cu + B + 1]
         self.plen = self._dev[o_pl:o_pl + B]
         self.plan = self._dev[o_plan:o_plan + self.plan_capacity]
-        self._n = ctypes.c_int32(0)
         p32 = lambda a: _ptr(a, ctypes.c_int32)
         self._p = {"tok": p32(self.tokens), "cut": _ptr(self.cu_tokens, ctypes.c_int64), "bt": p32(self.bt_host),
                    "cu": p32(self.cu_host), "pl": p32(self.plen_host), "plan": p32(self.plan_host)}
@@ -615,24 +646,25 @@ class BatchRunner:
     def total_rows(self) -> int:
         return int(self.cu_host[-1])
 
+    def _plan(self) -> None:
+        p = self._p
+        _check(_lib.cw_suffix_prefill_plan(p["cu"], p["pl"], self.batch, self.num_q_heads, self.num_kv_heads,
+                                           self.head_dim, 1, p["plan"], self.plan_capacity))
+        self.plan_words = PLAN_HEADER + PLAN_ENTRY * int(self.plan_host[HDR_ENTRIES])
+
     def schedule(self, pool: Pool) -> None:
-        """cw_schedule_batch into the host buffers, then the tile plan."""
+        """cw_schedule_batch into the host buffers, then the attention plan."""
         p = self._p
         _check(_lib.cw_schedule_batch(pool.handle, p["tok"], p["cut"], self.batch, self.block_size, self.bt_stride,
                                       p["bt"], p["pl"], p["cu"]))
-        _check(_lib.cw_suffix_prefill_plan(p["cu"], p["pl"], self.batch, self.num_q_heads, self.num_kv_heads,
-                                           self.head_dim, p["plan"], self.plan_capacity, ctypes.byref(self._n)))
-        self.num_tiles = self._n.value
+        self._plan()
 
     def set_schedule(self, block_table, prefix_len, cu_suffix) -> None:
         """Use a given schedule instead of cw_schedule_batch (fixed-depth batches)."""
         self.bt_host[...] = block_table
         self.plen_host[...] = prefix_len
         self.cu_host[...] = cu_suffix
-        p = self._p
-        _check(_lib.cw_suffix_prefill_plan(p["cu"], p["pl"], self.batch, self.num_q_heads, self.num_kv_heads,
-                                           self.head_dim, p["plan"], self.plan_capacity, ctypes.byref(self._n)))
-        self.num_tiles = self._n.value
+        self._plan()
 
     def release(self, pool: Pool) -> None:
         p = self._p
@@ -641,7 +673,7 @@ class BatchRunner:
 
     def upload(self) -> None:
         """One asynchronous copy of the host schedule to the device buffer (current stream)."""
-        n = self._o_plan + 4 * max(self.num_tiles, 1)
+        n = self._o_plan + self.plan_words
         self._dev[:n].copy_(self._host[:n], non_blocking=True)
 
     def bind(self, q, k_new, v_new, k_cache, v_cache, out, softmax_scale: float, stream=None) -> None:
@@ -661,13 +693,13 @@ class BatchRunner:
                              p["cu"], p["pl"], self.batch, hkv, D, BLOCK_SIZE, k_cache.shape[0], s]
         self._attn_args = [q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), self.bt.data_ptr(), self.bt_stride,
                            self.cu.data_ptr(), self.plen.data_ptr(), p["cu"], p["pl"], self.batch, hq, hkv, D,
-                           BLOCK_SIZE, k_cache.shape[0], float(softmax_scale), self.plan.data_ptr(), 0,
+                           BLOCK_SIZE, k_cache.shape[0], float(softmax_scale), p["plan"], self.plan.data_ptr(),
                            out.data_ptr(), s]
         self._rows = (q.shape[0], k_new.shape[0], v_new.shape[0], out.shape[0])
 
     def check_device_copies(self) -> None:
         """Checks that the uploaded schedule equals the host one (synchronises)."""
-        n = 4 * max(self.num_tiles, 1)
+        n = self.plan_words
         _check_copies((("block_table", self.bt, self.bt_host), ("cu_suffix", self.cu, self.cu_host),
                        ("prefix_len", self.plen, self.plen_host), ("plan", self.plan[:n], self.plan_host[:n])))
 
@@ -683,7 +715,6 @@ class BatchRunner:
             raise ValueError("bound tensors do not match the scheduled suffix rows")
         if DEBUG_CHECK_COPIES:
             self.check_device_copies()
-        self._attn_args[17] = self.num_tiles
         _check(_lib.cw_suffix_prefill_attn(*self._attn_args))
 
 

@@ -21,7 +21,7 @@ def test_debug_check_of_device_copies(monkeypatch):
     out = cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale)
     torch.cuda.synchronize()
     assert torch.equal(out, ref)
-    db.meta.plan[3] += 1   # a tile's cost: unused by the kernels, so harmless if launched
+    db.meta.plan[12] += 1   # the header's work word: unused by the kernels, so harmless if launched
     sentinel = torch.full_like(out, 7.0)
     with pytest.raises(ValueError, match="plan"):
         cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale, out=sentinel)

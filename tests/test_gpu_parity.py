@@ -60,23 +60,30 @@ def _compare_full(db, out):
     _check(np.concatenate(outs), np.concatenate(exps), w.name)
 
 
-def _sample_rows(S, rng, n_random=48):
+def _sample_rows(S, rng, n_rows=96):
+    """About n_rows distinct suffix rows: the first and last rows, then half
+    block-boundary rows (first and last slot of a 16-token block), half uniform."""
     rows = {0, 1, S - 1, S - 2}
     for b in range(0, S, 16):
         rows.update({b, b + 15})
     rows = [x for x in rows if 0 <= x < S]
     rng.shuffle(rows)
-    rows = rows[:n_random] + list(rng.integers(0, S, size=n_random))
-    return sorted(set(int(x) for x in rows) | {0, S - 1})
+    picked = set(int(x) for x in rows[:n_rows // 2]) | {0, S - 1}
+    pool = rng.permutation(S)
+    for x in pool:
+        if len(picked) >= min(n_rows, S):
+            break
+        picked.add(int(x))
+    return sorted(picked)
 
 
-def _compare_sampled(db, out, requests, seed=0):
+def _compare_sampled(db, out, requests, seed=0, n_rows=96):
     rng = np.random.default_rng(seed)
     outs, exps = [], []
     for r in requests:
         c0, c1 = int(db.sched.cu_suffix[r]), int(db.sched.cu_suffix[r + 1])
         P = int(db.sched.prefix_len[r])
-        rows = _sample_rows(c1 - c0, rng)
+        rows = _sample_rows(c1 - c0, rng, n_rows)
         exps.append(OA.suffix_prefill_rows(db.q_host[r], db.logical_k[r], db.logical_v[r], P, db.scale, rows))
         outs.append(out[c0:c1][torch.as_tensor(rows, device=out.device)].float().cpu().numpy())
     _check(np.concatenate(outs), np.concatenate(exps), db.workload.name + " (sampled rows)")
@@ -187,8 +194,11 @@ def _ragged(hq, hkv, D, S, P, seed):
 
 
 @pytest.mark.parametrize("hq,hkv,D", [(4, 4, 64), (8, 2, 128), (32, 8, 128), (64, 8, 128), (28, 4, 128),
-                                      (16, 1, 64)])
+                                      (16, 1, 64), (32, 1, 64), (64, 1, 64), (128, 1, 64), (96, 3, 128)])
 def test_attention_ragged_shapes(hq, hkv, D):
+    """Ragged lengths (empty, single-row, partial-block and multi-tile suffixes)
+    at every tile shape: G = Hq / Hkv query heads share a tile of 256 / G
+    positions, from 256 positions (G = 1) down to 2 (G = 128)."""
     S = [1, 15, 16, 17, 600, 0, 33, 129]
     P = [0, 16, 48, 0, 1024, 32, 1008, 64]
     w = _ragged(hq, hkv, D, S, P, seed=hq + D)
@@ -250,10 +260,12 @@ def test_topk_sweep_sampled(frac):
 
 @pytest.mark.parametrize("hit", ["low", "high"])
 def test_long_context_70b_sampled(hit):
+    """Two requests x all 64 heads x 256 sampled rows each (first and last rows,
+    block boundaries, uniform rows)."""
     w = W.long_context(hit)
     _say(f"attention {w.name} P={w.prefix_lens[:4]}...")
     db = B.materialize(w, keep_host=[0, w.batch - 1], gen_device="cuda")
-    _compare_sampled(db, _run(db), [0, w.batch - 1])
+    _compare_sampled(db, _run(db), [0, w.batch - 1], n_rows=256)
     del db
     _cleanup()
 
@@ -283,4 +295,91 @@ def test_prebound_runner_matches_binding_path_bitwise():
     assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
     assert torch.equal(k2.view(torch.int16), db.k_cache.view(torch.int16))
     rn.release(pool)
+    _cleanup()
+
+
+# ------------------------------------------------------------------ out-of-pool table entries
+def _with_table(db, bt):
+    """The batch with another block table (host and device copies)."""
+    w = db.workload
+    db.sched.block_table = bt
+    db.meta = cw.BatchMeta(bt, db.sched.cu_suffix, db.sched.prefix_len, w.num_q_heads, w.num_kv_heads,
+                           w.head_dim, db.q.device)
+    return db
+
+
+def _corrupt_table(db):
+    """Entries -1, num_blocks and num_blocks + 7 inside requests' prompts:
+    prefix blocks of request 1 and 2, a suffix block of request 2."""
+    bt = db.sched.block_table.copy()
+    nb = db.sched.num_blocks
+    bt[1, 1] = -1
+    bt[1, 3] = nb
+    bt[2, 0] = nb + 7
+    P2 = int(db.sched.prefix_len[2])
+    bt[2, P2 // 16 + 1] = -1                      # a suffix block: its append is dropped
+    return bt
+
+
+def _oop_workload():
+    S = [40, 70, 100]
+    P = [32, 64, 96]
+    return _ragged(8, 2, 128, S, P, seed=77)
+
+
+def test_kv_append_drops_out_of_pool_writes_bit_exact():
+    w = _oop_workload()
+    db = B.materialize(w, keep_host=[])
+    db = _with_table(db, _corrupt_table(db))
+    _say(f"kv_append out-of-pool entries {w.name}")
+    kb, vb = _bits(db.k_cache), _bits(db.v_cache)
+    expect_k = OP.kv_append_image(kb, _bits(db.k_new), db.sched.block_table, db.sched.cu_suffix,
+                                  db.sched.prefix_len, w.block_size)
+    expect_v = OP.kv_append_image(vb, _bits(db.v_new), db.sched.block_table, db.sched.cu_suffix,
+                                  db.sched.prefix_len, w.block_size, layout="d_slot")
+    cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(db.k_cache), expect_k)
+    assert np.array_equal(_bits(db.v_cache), expect_v)
+    _cleanup()
+
+
+def test_attention_reads_out_of_pool_blocks_as_zeros():
+    """Against the oracle with the logical K/V rows of every out-of-pool block
+    of a request zeroed (prefix and suffix blocks alike)."""
+    w = _oop_workload()
+    db = B.materialize(w)
+    db = _with_table(db, _corrupt_table(db))
+    _say(f"attention out-of-pool entries {w.name}")
+    out = _run(db)
+    nb = db.sched.num_blocks
+    outs, exps = [], []
+    for r in range(w.batch):
+        c0, c1 = int(db.sched.cu_suffix[r]), int(db.sched.cu_suffix[r + 1])
+        P = int(db.sched.prefix_len[r])
+        row = db.sched.block_table[r]
+        k = OP.zero_out_of_pool_blocks(db.logical_k[r], row, nb)
+        v = OP.zero_out_of_pool_blocks(db.logical_v[r], row, nb)
+        exps.append(OA.suffix_prefill_attention(db.q_host[r], k, v, P, db.scale))
+        outs.append(out[c0:c1].float().cpu().numpy())
+    _check(np.concatenate(outs), np.concatenate(exps), w.name + " (out-of-pool entries)")
+    _cleanup()
+
+
+# ------------------------------------------------------------------ plan binding on the device
+def test_device_plan_of_another_batch_computes_nothing():
+    """A device plan whose header fingerprint is not the validated batch's: the
+    kernel writes nothing (the host copy passed validation)."""
+    w = W.tiny_single()
+    db = B.materialize(w, keep_host=[])
+    cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
+    db.meta.plan[2] += 1                        # fingerprint word of the device copy only
+    sentinel = torch.full_like(db.q, 7.0)
+    cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale, out=sentinel)
+    torch.cuda.synchronize()
+    assert torch.all(sentinel == 7.0)
+    db.meta.plan[2] -= 1
+    cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale, out=sentinel)
+    torch.cuda.synchronize()
+    assert not torch.all(sentinel == 7.0)
     _cleanup()

@@ -23,7 +23,7 @@ def test_exports_every_declared_symbol():
     lib = ctypes.CDLL(cw.LIB_PATH)
     for name in declared:
         assert hasattr(lib, name), name
-    assert cw.abi_version() == 2
+    assert cw.abi_version() == 3
 
 
 @pytest.mark.parametrize("n", [0, 1, 15, 16, 17, 100, 1408])
@@ -165,32 +165,63 @@ def test_schedule_batch_keeps_one_suffix_token_and_shares_within_batch():
     assert bt[0, 4:].tolist() == [-1] * 4
 
 
-def _plan_rows(plan, ntiles, cu, hkv, per):
-    seen = {}
-    for i in range(ntiles):
-        r, g, row0, cost = plan[4 * i:4 * i + 4]
-        if r < 0:
-            continue
+def _entries(plan):
+    """Real entries of a plan with their queue (workgroup) and queue position."""
+    grid, qlen = int(plan[cw.HDR_GRID]), int(plan[cw.HDR_QUEUE_LEN])
+    ents = cw.plan_entries(plan)
+    assert len(ents) == grid * qlen == plan[cw.HDR_ENTRIES]
+    out = []
+    for w in range(grid):
+        ended = False
+        for i in range(qlen):
+            e = ents[i * grid + w]
+            if e[cw.ENT_R] < 0:
+                ended = True
+                continue
+            assert not ended, "a real entry after the end of its queue"
+            out.append((w, i, e))
+    return out
+
+
+def _check_plan(plan, cu, P, hq, hkv, splits=1):
+    """Every (request, KV head, row) is covered by exactly one tile, and each
+    tile's 64-key steps by its split runs exactly once, in order; the fields
+    are the batch's own."""
+    per = cw.TILE_ROWS // (hq // hkv)
+    rows, runs = {}, {}
+    for w, i, e in _entries(plan):
+        r, g, row0, nv, cu0, p, L, kb, ke, sp = (int(x) for x in e[:10])
         S = cu[r + 1] - cu[r]
-        for row in range(row0, min(S, row0 + per)):
-            key = (r, g, row)
-            seen[key] = seen.get(key, 0) + 1
-    return seen
+        assert 0 <= g < hkv and row0 % per == 0 and nv == min(per, S - row0) and nv >= 1
+        assert cu0 == cu[r] and p == P[r] and L == P[r] + S
+        n = -(-(p + row0 + nv) // 64)
+        run = -(-n // splits)
+        assert 0 <= sp < splits and kb == min(n, sp * run) and ke == min(n, kb + run)
+        runs.setdefault((r, g, row0), []).append((sp, kb, ke, n))
+        if sp == 0:
+            for row in range(row0, row0 + nv):
+                rows[(r, g, row)] = rows.get((r, g, row), 0) + 1
+    assert len(rows) == int(np.sum(np.diff(cu))) * hkv and set(rows.values()) <= {1}
+    for key, rr in runs.items():
+        rr.sort()
+        assert [x[0] for x in rr] == list(range(splits))
+        n = rr[0][3]
+        steps = [t for _, kb, ke, _ in rr for t in range(kb, ke)]
+        assert steps == list(range(n))
+    return per
 
 
-def _grouped(plan, n, hkv):
-    """True when each (request, KV head) pair sits on one partition (i % 8)."""
+def _grouped(plan):
+    """True when each (request, KV head) pair's entries sit on one partition (queue % 8)."""
     part = {}
-    for i in range(n):
-        if plan[4 * i] >= 0:
-            key = (plan[4 * i], plan[4 * i + 1])
-            if part.setdefault(key, i % 8) != i % 8:
-                return False
+    for w, i, e in _entries(plan):
+        if part.setdefault((int(e[0]), int(e[1])), w % 8) != w % 8:
+            return False
     return len(part) >= 32
 
 
-@pytest.mark.parametrize("shape", [(4, 1), (32, 8), (64, 8), (28, 4)])
-def test_plan_covers_every_row_once(shape):
+@pytest.mark.parametrize("shape", [(4, 1), (32, 8), (64, 8), (28, 4), (128, 1)])
+def test_plan_covers_every_row_and_step_once(shape):
     hq, hkv = shape
     rng = np.random.default_rng(hq)
     for B in (1, 3, 16, 40):
@@ -198,70 +229,75 @@ def test_plan_covers_every_row_once(shape):
         S[0] = max(S[0], 1)
         P = rng.integers(0, 60, size=B) * 16
         cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
-        plan, n = cw.suffix_prefill_plan(cu, P, hq, hkv, 128)
-        per = cw.TILE_ROWS // (hq // hkv)
-        seen = _plan_rows(plan, n, cu, hkv, per)
-        assert len(seen) == int(S.sum()) * hkv and set(seen.values()) == {1}
-        real = [plan[4 * i:4 * i + 4] for i in range(n) if plan[4 * i] >= 0]
-        assert len(real) == sum(math.ceil(s / per) for s in S) * hkv
-        for t in real:
-            r, g, row0, cost = t
-            kv_end = P[r] + row0 + min(per, S[r] - row0)
-            assert cost == math.ceil(kv_end / 64)
-        if _grouped(plan, n, hkv):
-            # per L2-partition queue (entries i % 8): pairs contiguous, each pair's
-            # tiles heaviest first, pairs by non-increasing total cost
-            for x in range(8):
-                q = [tuple(plan[4 * i:4 * i + 4]) for i in range(x, n, 8) if plan[4 * i] >= 0]
-                pairs, totals = [], {}
-                for r_, g_, row0, cost in q:
-                    if not pairs or pairs[-1] != (r_, g_):
-                        assert (r_, g_) not in totals
-                        pairs.append((r_, g_))
-                    totals[(r_, g_)] = totals.get((r_, g_), 0) + cost
-                for pr in pairs:
-                    cs = [c for r_, g_, _, c in q if (r_, g_) == pr]
-                    assert cs == sorted(cs, reverse=True)
-                tl = [totals[pr] for pr in pairs]
-                assert tl == sorted(tl, reverse=True)
-        else:
-            costs = [t[3] for t in real]
-            assert costs == sorted(costs, reverse=True)
+        for splits in (1, 3):
+            plan = cw.suffix_prefill_plan(cu, P, hq, hkv, 128, splits)
+            assert plan[0] == 0x33505743 and plan[cw.HDR_SPLITS] == splits
+            per = _check_plan(plan, cu, P, hq, hkv, splits)
+            ents = _entries(plan)
+            assert len(ents) == sum(math.ceil(s / per) for s in S) * hkv * splits
+            assert plan[cw.HDR_GRID] == min(256, len(ents))
+
+
+def test_plan_queues_are_balanced_longest_first():
+    """Each queue runs its entries heaviest first, and no queue carries more
+    than the lightest queue plus its heaviest entry (list scheduling)."""
+    rng = np.random.default_rng(5)
+    S = rng.integers(1, 1400, size=16)
+    P = rng.integers(0, 20, size=16) * 64
+    cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
+    plan = cw.suffix_prefill_plan(cu, P, 32, 8, 128)
+    load, heavy = {}, {}
+    last = {}
+    for w, i, e in _entries(plan):
+        c = int(e[cw.ENT_KEND] - e[cw.ENT_KBEG]) + 1
+        assert c <= last.get(w, 1 << 30)
+        last[w] = c
+        load[w] = load.get(w, 0) + c
+        heavy[w] = max(heavy.get(w, 0), c)
+    assert len(load) == 256
+    assert max(load.values()) <= min(load.values()) + max(heavy.values())
 
 
 @pytest.mark.parametrize("grouped", [False, True])
 def test_plan_writes_exactly_plan_words(grouped):
     """The plan fills exactly the size cw_suffix_prefill_plan_words reports, with
-    empty requests anywhere in the batch (guard words after the buffer stay intact)."""
+    empty requests anywhere in the batch (guard words after the buffer stay
+    intact); a smaller buffer is refused."""
     B = 40 if grouped else 3
     S = np.array([0, 5, 0, 700, 33, 0] * 7, dtype=np.int32)[:B]
     P = np.arange(B, dtype=np.int32) % 5 * 16
     cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
     cu_a, cu_p = _arr(cu)
     pl_a, pl_p = _arr(P)
-    words = cw.lib().cw_suffix_prefill_plan_words(cu_p, pl_p, B, 32, 8, 128)
-    assert words > 0
+    words = cw.lib().cw_suffix_prefill_plan_words(cu_p, pl_p, B, 32, 8, 128, 1)
+    assert words > 16
     buf = np.full(words + 256, -7, dtype=np.int32)
-    n = ctypes.c_int32(0)
-    st = cw.lib().cw_suffix_prefill_plan(cu_p, pl_p, B, 32, 8, 128,
-                                         buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), words,
-                                         ctypes.byref(n))
-    assert st == cw.CW_OK and 4 * n.value == words
+    bp = buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    assert cw.lib().cw_suffix_prefill_plan(cu_p, pl_p, B, 32, 8, 128, 1, bp, words - 1) == cw.CW_EINVAL
+    assert cw.lib().cw_suffix_prefill_plan(cu_p, pl_p, B, 32, 8, 128, 1, bp, words) == cw.CW_OK
+    assert words == 16 + 16 * buf[cw.HDR_ENTRIES]
     assert (buf[words:] == -7).all()
-    assert _grouped(buf[:words], n.value, 8) == grouped
-    seen = _plan_rows(buf, n.value, cu, 8, cw.TILE_ROWS // 4)
-    assert len(seen) == int(S.sum()) * 8 and set(seen.values()) == {1}
+    assert _grouped(buf[:words]) == grouped
+    _check_plan(buf[:words], cu, P, 32, 8)
 
 
 def test_plan_groups_pairs_on_one_partition():
     cu = np.arange(0, 17 * 576, 576, dtype=np.int32)
     P = np.full(16, 832, np.int32)
-    plan, n = cw.suffix_prefill_plan(cu, P, 32, 8, 128)
-    part = {}
-    for i in range(n):
-        r, g = plan[4 * i], plan[4 * i + 1]
-        if r >= 0:
-            assert part.setdefault((r, g), i % 8) == i % 8
+    assert _grouped(cw.suffix_prefill_plan(cu, P, 32, 8, 128))
+
+
+def test_plan_check_words_bind_entries_to_the_batch():
+    """Each entry's check word is the library's hash of its fields seeded with
+    the batch fingerprint: plans of two batches that differ in one prefix
+    length differ in every real entry's check word."""
+    cu = np.array([0, 300, 900], np.int32)
+    a = cw.suffix_prefill_plan(cu, [0, 64], 32, 8, 128)
+    b = cw.suffix_prefill_plan(cu, [0, 80], 32, 8, 128)
+    assert tuple(a[2:4]) != tuple(b[2:4])
+    ea, eb = cw.plan_entries(a), cw.plan_entries(b)
+    real = ea[:, 0] >= 0
+    assert (ea[real, 15] != eb[real, 15]).all()
 
 
 def _dummy():
@@ -273,15 +309,27 @@ def _arr(x):
     return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
 
 
-def _attn(cu, plen, hq=32, hkv=8, d=128, bs=16, stride=100, scale=0.1, ntiles=None, nb=100):
+def _attn(cu, plen, hq=32, hkv=8, d=128, bs=16, stride=100, scale=0.1, nb=100, plan=None, split=False,
+          ws_bytes=None, workspace=True):
+    """Calls an attention entry point with dummy device pointers (never
+    dereferenced: every case here returns before a launch)."""
     cu_a, cu_p = _arr(cu)
     pl_a, pl_p = _arr(plen)
-    if ntiles is None:
-        per = max(1, cw.TILE_ROWS // max(1, hq // hkv))
-        ntiles = sum(math.ceil((cu[i + 1] - cu[i]) / per) for i in range(len(plen))) * hkv
+    if plan is None:
+        try:
+            plan = cw.suffix_prefill_plan(cu, plen, hq, hkv, d)
+        except cw.CwError:
+            plan = np.zeros(16, np.int32)
+    plan = np.ascontiguousarray(plan, np.int32)
+    pp = plan.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
     d_ = _dummy()
-    return cw.lib().cw_suffix_prefill_attn(d_, d_, d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d,
-                                           bs, nb, scale, d_, ntiles, d_, None)
+    if not split:
+        return cw.lib().cw_suffix_prefill_attn(d_, d_, d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d,
+                                               bs, nb, scale, pp, d_, d_, None)
+    if ws_bytes is None:
+        ws_bytes = max(0, cw.lib().cw_suffix_prefill_split_workspace_bytes(cu[-1], hq, d, int(max(1, plan[5]))))
+    return cw.lib().cw_suffix_prefill_attn_split(d_, d_, d_, d_, stride, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d,
+                                                 bs, nb, scale, pp, d_, d_ if workspace else None, ws_bytes, d_, None)
 
 
 def _append(cu, plen, hkv=8, d=128, bs=16, stride=100, nb=100):
@@ -301,7 +349,12 @@ def test_device_entry_points_validate_before_launch():
     assert _attn([0, 10], [0], d=96) == U                 # head_dim
     assert _attn([0, 10], [0], bs=32) == U                # block size
     assert _attn([0, 10], [0], hq=256, hkv=1) == U        # group > 128
-    assert _attn([0, 10], [0], ntiles=3) == E             # plan does not match
+    other = cw.suffix_prefill_plan([0, 10], [16], 32, 8, 128)
+    assert _attn([0, 10], [0], plan=other) == E           # a plan of another batch
+    assert "another batch" in cw.last_error()
+    assert _attn([0, 10], [0], plan=cw.suffix_prefill_plan([0, 10], [0], 16, 4, 128)) == E   # other heads
+    assert _attn([0, 10], [0], plan=np.zeros(16, np.int32)) == E      # not a plan
+    assert _attn([0, 10], [0], plan=cw.suffix_prefill_plan([0, 10], [0], 32, 8, 128, 2)) == E   # splits
     assert _attn([0, 10], [0], scale=float("nan")) == E
     assert _attn([0, 10], [0], scale=-1.0) == E
     assert _attn([0, 10], [0], nb=0) == E
@@ -311,7 +364,7 @@ def test_device_entry_points_validate_before_launch():
     assert _append([0, 10], [0], bs=8) == U
     assert _append([0, 10], [0], hkv=0) == E
     assert _append([0, 1000], [16 * 90]) == E
-    assert _attn([0, 0], [0], ntiles=0) == cw.CW_OK       # nothing to do: no launch
+    assert _attn([0, 0], [0]) == cw.CW_OK                 # nothing to do: no launch
     assert _append([0, 0], [16]) == cw.CW_OK
 
 
@@ -342,16 +395,11 @@ def test_qkv_rope_append_validates_before_launch():
 
 
 def _split(cu, plen, splits=2, ws_bytes=None, hq=32, hkv=8, d=128, workspace=True):
-    cu_a, cu_p = _arr(cu)
-    pl_a, pl_p = _arr(plen)
-    per = max(1, cw.TILE_ROWS // max(1, hq // hkv))
-    ntiles = sum(math.ceil((cu[i + 1] - cu[i]) / per) for i in range(len(plen))) * hkv
-    if ws_bytes is None:
-        ws_bytes = max(0, cw.lib().cw_suffix_prefill_split_workspace_bytes(cu[-1], hq, d, max(1, min(splits, 64))))
-    d_ = _dummy()
-    return cw.lib().cw_suffix_prefill_attn_split(d_, d_, d_, d_, 100, d_, d_, cu_p, pl_p, len(plen), hq, hkv, d, 16,
-                                                 100, 0.1, d_, ntiles, splits, d_ if workspace else None, ws_bytes,
-                                                 d_, None)
+    try:
+        plan = cw.suffix_prefill_plan(cu, plen, hq, hkv, d if d in (64, 128) else 128, splits)
+    except cw.CwError:
+        return cw.CW_EINVAL if not (1 <= splits <= 64) else None
+    return _attn(cu, plen, hq=hq, hkv=hkv, d=d, plan=plan, split=True, ws_bytes=ws_bytes, workspace=workspace)
 
 
 def test_split_workspace_size():
@@ -430,7 +478,7 @@ def test_debug_check_of_device_copies():
     with pytest.raises(ValueError, match="cu_suffix"):
         meta.check_device_copies()
     meta.cu[2] = 30
-    meta.plan[3] += 1
+    meta.plan[20] += 1
     with pytest.raises(ValueError, match="plan"):
         meta.check_device_copies()
     meta.plan = None
