@@ -37,6 +37,11 @@ HIP_FLAGS = [
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra"]
+# Per-source extra flags. The attention kernel's step has uniform (wave-wide)
+# branches only; structurizing them makes the register allocator keep two
+# copies of the 64-register output accumulator across the branch arms, which
+# overflows the 256-register budget of two waves per SIMD.
+EXTRA_FLAGS = {"cw_kernels.hip": ["-mllvm", "-structurizecfg-skip-uniform-regions=true"]}
 
 
 def _run(cmd):
@@ -60,7 +65,7 @@ def build(verbose: bool = False) -> str:
                 print(out)
         for src in HIP_SOURCES:
             obj = os.path.join(tmp, src + ".o")
-            out = _run([HIPCC, *HIP_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
+            out = _run([HIPCC, *HIP_FLAGS, *EXTRA_FLAGS.get(src, []), *incs, "-c", os.path.join(CSRC, src), "-o", obj])
             objs.append(obj)
             if verbose and out:
                 print(out)
