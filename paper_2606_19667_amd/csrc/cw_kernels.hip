@@ -480,6 +480,15 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 
+  // Q of the next entry, loaded (raw bf16) during the current entry's last
+  // step so that an entry starts without waiting for its queries.
+  u32x4 qn[KS];
+  bool q_ready = false;
+  // This lane's query column inside a tile.
+  const int m = wave * 32 + l32;
+  const int hh = m / a.per_tile;
+  const int pos = m - hh * a.per_tile;
+
   for (int e = blockIdx.x; e < a.num_entries; e += grid) {
     cint32_t* en = ents + int64_t(e) * kEntryWords;
     int32_t f[cw::kEntFields];
@@ -487,16 +496,29 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     for (int i = 0; i < cw::kEntFields; ++i) f[i] = en[i];
     // the end of the queue, or an entry that is not the one the planner wrote
     if (f[cw::kEntR] < 0 || uint32_t(en[cw::kEntCheck]) != cw::entry_check(a.fp_lo, a.fp_hi, f)) break;
+    // the next entry's rows, for the Q prefetch (valid: a whole entry with keys)
+    bool next_q = false;
+    int64_t qrow_n = 0;
+    int head_n = 0;
+    bool row_ok_n = false;
+    // (not on the split path, whose kernel has no registers to spare for it)
+    if (!SPLIT && e + grid < a.num_entries) {
+      cint32_t* nx = ents + int64_t(e + grid) * kEntryWords;
+      int32_t fn[cw::kEntFields];
+#pragma unroll
+      for (int i = 0; i < cw::kEntFields; ++i) fn[i] = nx[i];
+      next_q = fn[cw::kEntR] >= 0 && fn[cw::kEntKend] > fn[cw::kEntKbeg] &&
+               uint32_t(nx[cw::kEntCheck]) == cw::entry_check(a.fp_lo, a.fp_hi, fn);
+      row_ok_n = (hh < a.group) && (pos < fn[cw::kEntNvalid]);
+      qrow_n = int64_t(fn[cw::kEntCu0]) + fn[cw::kEntRow0] + pos;
+      head_n = fn[cw::kEntG] * a.group + hh;
+    }
     const int g = f[cw::kEntG], row0 = f[cw::kEntRow0], nvalid = f[cw::kEntNvalid];
     const int cu0 = f[cw::kEntCu0], P = f[cw::kEntP];
     const int kbeg = f[cw::kEntKbeg], kend = f[cw::kEntKend];
     const int split = SPLIT ? f[cw::kEntSplit] : 0;
     const int nsteps = kend - kbeg;
 
-    // This lane's query column.
-    const int m = wave * 32 + l32;
-    const int hh = m / a.per_tile;
-    const int pos = m - hh * a.per_tile;
     const bool row_ok = (hh < a.group) && (pos < nvalid);
     const int qpos = P + row0 + pos;  // keys 0 .. qpos are visible
     const int64_t qrow = int64_t(cu0) + row0 + pos;
@@ -517,13 +539,25 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     }
 
     bf16x8 qf[KS];
-    if (row_ok) {
-      const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow * a.hq + head) * D);
+    if constexpr (SPLIT) {
+      if (row_ok) {
+        const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow * a.hq + head) * D);
 #pragma unroll
-      for (int s = 0; s < KS; ++s) qf[s] = scale_bf16x8(qp[2 * s + half], a.c_log2);
+        for (int s = 0; s < KS; ++s) qf[s] = scale_bf16x8(qp[2 * s + half], a.c_log2);
+      } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+      }
     } else {
+      if (!q_ready && row_ok) {
+        const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow * a.hq + head) * D);
 #pragma unroll
-      for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+        for (int s = 0; s < KS; ++s) qn[s] = qp[2 * s + half];
+      }
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        qf[s] = row_ok ? scale_bf16x8(qn[s], a.c_log2) : __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+      q_ready = false;
     }
 
     // Compute works on 32-key halves of a staged 64-key step ("sub-steps"):
@@ -701,6 +735,14 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       step_barrier(direct);
     };
     for (int j = 0; j < nsteps; ++j) {
+      if (j == nsteps - 1 && next_q) {   // the next entry's Q (qf stays in use)
+        if (row_ok_n) {
+          const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow_n * a.hq + head_n) * D);
+#pragma unroll
+          for (int s = 0; s < KS; ++s) qn[s] = qp[2 * s + half];
+        }
+        q_ready = true;
+      }
       step(j);
       ++p;
     }
@@ -965,3 +1007,4 @@ extern "C" cw_status cw_lse_merge(const void* partial_o, const void* partial_lse
   return launch_merge(static_cast<const float*>(partial_o), static_cast<const float*>(partial_lse), num_parts,
                       rows, head_dim, out, static_cast<hipStream_t>(stream));
 }
+
