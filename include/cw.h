@@ -346,6 +346,32 @@ cw_status cw_suffix_prefill_attn_split(const void* q, const void* k_cache, const
                                        void* workspace, int64_t workspace_bytes, void* out, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Device: cw_suffix_prefill_attn_split without a workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation). Same arguments, result and errors
+ * as cw_suffix_prefill_attn_split, without workspace / workspace_bytes: the
+ * partial results go to a device array built into the library, of
+ * cw_noalloc_scratch_bytes() bytes (64 MiB), which every GPU the library runs
+ * on holds until the process ends. The call allocates nothing.
+ *   - CW_EINVAL when the batch needs more than that:
+ *     cw_suffix_prefill_split_workspace_bytes(total_s, Hq, D, num_splits) >
+ *     cw_noalloc_scratch_bytes().
+ *   - Every call on one GPU shares that GPU's array: calls that overlap in time
+ *     on one GPU (other streams, other threads) race and may corrupt each
+ *     other's results. Calls on one stream are ordered and safe. The array
+ *     keeps the last call's contents; nothing in it needs to start at zero.
+ *   - CW_EHIP if the array's device address cannot be obtained. */
+int64_t cw_noalloc_scratch_bytes(void);
+cw_status cw_suffix_prefill_attn_split_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                               const int32_t* block_table, int32_t bt_stride,
+                                               const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev,
+                                               const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                               int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                               int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                                               float softmax_scale, const int32_t* plan_host,
+                                               const int32_t* plan_dev, void* out, void* stream);
+
+/* ------------------------------------------------------------------------
  * Device: merge of attention results computed over disjoint key sets (the
  * pieces of cw_suffix_prefill_attn_split; also how partial results over a
  * prefix split across GPUs would be combined). Softmax over a union of key

@@ -27,6 +27,7 @@ constexpr int kMaxGroup = 128;   // query heads per KV head supported
 
 constexpr int kNumCu = 256;      // compute units: the attention grid's persistent workgroups
 constexpr int kMaxSplits = 64;   // key runs per tile on the split path
+constexpr int64_t kNoAllocScratchBytes = int64_t(64) << 20;   // scratch of the allocation-free split call
 
 // Suffix positions covered by one tile for a GQA group of `group` query heads.
 inline int tile_positions(int group) { return kTileRows / group; }

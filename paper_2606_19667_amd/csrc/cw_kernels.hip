@@ -25,6 +25,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include <string>
 #include <type_traits>
 
@@ -1008,3 +1009,76 @@ extern "C" cw_status cw_lse_merge(const void* partial_o, const void* partial_lse
                       rows, head_dim, out, static_cast<hipStream_t>(stream));
 }
 
+// ---------------------------------------------------------------------------
+// Split attention without allocation. The split path's partial results (fp32
+// O per run and row, and the per-row log-sum-exp) go to a file-scope device
+// array instead of a caller workspace, for callers that cannot allocate. Each
+// GPU the library runs on holds its own copy of the array for the life of the
+// process. The host takes the array's device address once per device (with
+// that device current) through hipGetSymbolAddress and passes that address to
+// the kernels; the array's name itself is never used as a device pointer on
+// the host.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int64_t kScratchBytes = cw::kNoAllocScratchBytes;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (taken on first use).
+cw_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return cw::fail(CW_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return cw::fail(CW_EUNSUPPORTED, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return cw::fail(CW_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CW_OK;
+}
+
+}  // namespace
+
+extern "C" int64_t cw_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+extern "C" cw_status cw_suffix_prefill_attn_split_noalloc(
+    const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table, int32_t bt_stride,
+    const int32_t* cu_suffix_dev, const int32_t* prefix_len_dev, const int32_t* cu_suffix_host,
+    const int32_t* prefix_len_host, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+    int32_t block_size, int32_t num_blocks, float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev,
+    void* out, void* stream) {
+  AttnLaunch L;
+  cw_status st = check_attn("suffix_prefill_attn_split_noalloc", q, k_cache, v_cache, block_table, bt_stride,
+                            cu_suffix_dev, prefix_len_dev, cu_suffix_host, prefix_len_host, batch, num_q_heads,
+                            num_kv_heads, head_dim, block_size, num_blocks, softmax_scale, plan_host, plan_dev,
+                            out, &L);
+  if (st != CW_OK) return st;
+  const int64_t need = cw_suffix_prefill_split_workspace_bytes(L.rows, num_q_heads, head_dim, L.splits);
+  if (need > kScratchBytes)
+    return cw::fail(CW_EINVAL, "suffix_prefill_attn_split_noalloc: the batch needs " + std::to_string(need) +
+                                   " bytes of partial results; the built-in scratch holds " +
+                                   std::to_string(kScratchBytes));
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != CW_OK) return st;
+  if (L.rows == 0 || L.grid == 0) return cw::ok();
+  auto* s = static_cast<hipStream_t>(stream);
+  // Every part of every row is written by the split kernel (empty runs write
+  // zeros and -inf) before the merge reads it, so nothing needs clearing.
+  L.args.part_o = static_cast<float*>(ws);
+  L.args.part_lse = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) +
+                                             split_lse_offset(L.args.part_rows, head_dim, L.splits));
+  launch_attn<true>(head_dim, L, s);
+  st = check_launch("suffix_prefill_attn_split_noalloc launch");
+  if (st != CW_OK) return st;
+  return launch_merge(L.args.part_o, L.args.part_lse, L.splits, L.args.part_rows, head_dim, out, s);
+}

@@ -78,6 +78,10 @@ def _load() -> ctypes.CDLL:
                                                 _i32, _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp,
                                                 _vp, _i64, _vp, _vp]),
         "cw_lse_merge": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp, _vp]),
+        "cw_noalloc_scratch_bytes": (_i64, []),
+        "cw_suffix_prefill_attn_split_noalloc": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
+                                                        _i32, _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp,
+                                                        _vp, _vp]),
         "cw_tree_create": (_i32, [_i32, ctypes.POINTER(_vp)]),
         "cw_tree_destroy": (None, [_vp]),
         "cw_tree_num_nodes": (_i64, [_vp]),
@@ -105,6 +109,7 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_release_batch", "cw_kv_append", "cw_suffix_prefill_plan_words",
             "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
             "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge",
+            "cw_noalloc_scratch_bytes", "cw_suffix_prefill_attn_split_noalloc",
             "cw_tree_create", "cw_tree_destroy", "cw_tree_num_nodes", "cw_tree_insert",
             "cw_tree_mark_stale", "cw_tree_order", "cw_rope_table", "cw_qkv_rope_append",
             "cw_probe_mfma_bf16_flops", "cw_probe_mfma_bf16")
@@ -559,6 +564,41 @@ def suffix_prefill_attn_split(meta: BatchMeta, q: torch.Tensor, k_cache: torch.T
         meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
         k_cache.shape[0], float(softmax_scale), meta._hp(plan_host), _dev(plan_dev, torch.int32, "plan"),
         _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out
+
+
+def noalloc_scratch_bytes() -> int:
+    """Size of the library's built-in scratch for the allocation-free split call."""
+    return int(_lib.cw_noalloc_scratch_bytes())
+
+
+def suffix_prefill_attn_split_noalloc(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
+                                      v_cache: torch.Tensor, softmax_scale: float, num_splits: int | None = None,
+                                      out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """cw_suffix_prefill_attn_split_noalloc: the split path with the library's
+    built-in scratch instead of a workspace (the call allocates no device
+    memory; `out` must be given by callers that cannot allocate)."""
+    if DEBUG_CHECK_COPIES:
+        meta.check_device_copies()
+    hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
+    if num_splits is None:
+        num_splits = split_count(meta)
+    if tuple(q.shape) != (meta.total_rows, hq, D):
+        raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
+    if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+    if out is None:
+        out = torch.empty_like(q)
+    elif tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must have q's shape")
+    plan_host, plan_dev = meta.split_plan(int(num_splits))
+    _check(_lib.cw_suffix_prefill_attn_split_noalloc(
+        _dev(q, torch.bfloat16, "q"), _dev(k_cache, torch.bfloat16, "k_cache"),
+        _dev(v_cache, torch.bfloat16, "v_cache"), _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
+        _dev(meta.cu, torch.int32, "cu_suffix"), _dev(meta.plen, torch.int32, "prefix_len"),
+        meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
+        k_cache.shape[0], float(softmax_scale), meta._hp(plan_host), _dev(plan_dev, torch.int32, "plan"),
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
