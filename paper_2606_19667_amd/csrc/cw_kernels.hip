@@ -561,28 +561,31 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       q_ready = false;
     }
 
-    // Compute works on 32-key halves of a staged 64-key step ("sub-steps"):
-    // the score accumulator of a half is one 32x32 MFMA tile, so two of them
-    // (the current and the next) take 32 registers.
-    //
-    // Causal mask of the half starting at key k0 (sc holds keys k0 + (e / 8) 16 +
-    // half 8 + e % 8; the lane term moves to the limit so the per-element terms
-    // stay immediates).
-    auto mask = [&](f32x16& sc, int k0) __attribute__((always_inline)) {
+    // Causal mask of the step starting at key k0: element e of accumulator h
+    // holds key k0 + 32 h + (e / 8) 16 + half 8 + e % 8; the lane term moves to
+    // the limit so that the per-element terms stay immediates.
+    auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
       const int lim = qpos - k0 - half * 8;
 #pragma unroll
-      for (int e2 = 0; e2 < 16; ++e2)
-        if ((e2 >> 3) * 16 + (e2 & 7) > lim) sc[e2] = -INFINITY;
-    };
-    // Maximum of the row over a half's 32 keys (this lane's 16 and lane ^ 32's).
-    auto rowmax = [&](const f32x16& sc) __attribute__((always_inline)) -> float {
-      float x = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int e2 = 3; e2 < 15; e2 += 2) x = fmaxf(fmaxf(x, sc[e2]), sc[e2 + 1]);
-      return max_pair32(fmaxf(x, sc[15]));
+        for (int e2 = 0; e2 < 16; ++e2)
+          if (h * 32 + (e2 >> 3) * 16 + (e2 & 7) > lim) sc[h][e2] = -INFINITY;
+    };
+    // Maximum of the row over a step's 64 keys (this lane's 32 and lane ^ 32's).
+    auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) -> float {
+      float x = fmaxf(fmaxf(sc[0][0], sc[0][1]), sc[0][2]);
+      float y = fmaxf(fmaxf(sc[1][0], sc[1][1]), sc[1][2]);
+#pragma unroll
+      for (int e2 = 3; e2 < 15; e2 += 2) {
+        x = fmaxf(fmaxf(x, sc[0][e2]), sc[0][e2 + 1]);
+        y = fmaxf(fmaxf(y, sc[1][e2]), sc[1][e2 + 1]);
+      }
+      x = fmaxf(fmaxf(x, sc[0][15]), sc[1][15]);
+      return max_pair32(fmaxf(x, y));
     };
 
-    float l_run = 0.f;   // this lane's partial row sum (its 16 keys per half)
+    float l_run = 0.f;   // this lane's partial row sum (its 32 keys per step)
     const bf16x2 ones{(__bf16)1.0f, (__bf16)1.0f};
     f32x16 oacc[DT];
 #pragma unroll
@@ -590,100 +593,112 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     f32x16 mneg;   // -m in every element: the start of each S accumulator
     float mx = 0.f;   // row maximum of the current S (relative to the base)
 
-    // K operand of QK MFMA s (k-step s over D) for half h of the stage at kb;
-    // V operand of PV MFMA i for half h: 16-key slice kk = i / DT of the half
-    // (block 2 h + kk), output tile t = i % DT.
-    auto rdk = [&](int kb, int h, int s) __attribute__((always_inline)) -> bf16x8 {
-      return rd16(kb + k_off[s] + h * 32 * RB);
+    // K operand of QK MFMA i (k-step i / 2 over D, 32-key half i % 2) of the
+    // stage at kb; V operand of PV MFMA i (16-key slice i / DT, output tile
+    // i % DT) of the stage at vb.
+    auto rdk = [&](int kb, int i) __attribute__((always_inline)) -> bf16x8 {
+      return rd16(kb + k_off[i >> 1] + (i & 1) * 32 * RB);
     };
-    auto rdv = [&](int vb, int h, int i) __attribute__((always_inline)) -> bf16x8 {
-      return rd16(vb + (2 * h + i / DT) * BLK + (i % DT) * 1024);
+    auto rdv = [&](int vb, int i) __attribute__((always_inline)) -> bf16x8 {
+      return rd16(vb + (i / DT) * BLK + (i % DT) * 1024);
     };
-    // S^T = K Q^T of one half (no other work), accumulator from zero.
-    auto qk_alone = [&](int kb, int h, f32x16& sc) __attribute__((always_inline)) {
+    // S^T = K Q^T of a step (no other work), accumulators from zero.
+    auto qk_alone = [&](int kb, f32x16 (&sc)[2]) __attribute__((always_inline)) {
+      constexpr int N = 2 * KS;
       bf16x8 kf[3];
 #pragma unroll
-      for (int i = 0; i < 3 && i < KS; ++i) kf[i] = rdk(kb, h, i);
+      for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, i);
 #pragma unroll
-      for (int i = 0; i < KS; ++i) {
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i], i == 0 ? f32x16{} : sc, 0, 0, 0);
-        if (i + 3 < KS) kf[i % 3] = rdk(kb, h, i + 3);
+      for (int i = 0; i < N; ++i) {
+        sc[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? f32x16{} : sc[i & 1], 0, 0, 0);
+        if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
       }
     };
-    // Probabilities of element pair i (of 8) of a half: 2^(s - m) for two keys,
+    // Probabilities of element pair i (of 16) of S: 2^(s - m) for two keys,
     // packed to bf16, and their sum added to ls.
-    auto prob_pair = [&](const f32x16& sc, int i, float& ls) __attribute__((always_inline)) -> uint32_t {
-      const uint32_t w = pack_bf16x2(__builtin_amdgcn_exp2f(sc[2 * i]), __builtin_amdgcn_exp2f(sc[2 * i + 1]));
+    auto prob_pair = [&](const f32x16 (&sc)[2], int i, float& ls) __attribute__((always_inline)) -> uint32_t {
+      const int kk = i >> 2, jj = i & 3, h = kk >> 1, e = (kk & 1) * 8 + 2 * jj;
+      const uint32_t w = pack_bf16x2(__builtin_amdgcn_exp2f(sc[h][e]), __builtin_amdgcn_exp2f(sc[h][e + 1]));
       ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, ls, false);
       return w;
     };
-    auto pack_pb = [&](const uint32_t (&w)[8], bf16x8 (&pb)[2]) __attribute__((always_inline)) {
+    auto pack_pb = [&](const uint32_t (&w)[16], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk], w[4 * kk + 1], w[4 * kk + 2], w[4 * kk + 3]});
+      for (int kk = 0; kk < 4; ++kk) pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk], w[4 * kk + 1], w[4 * kk + 2], w[4 * kk + 3]});
     };
-    // Phase A of a sub-step: the next half's S = K Q^T (KS MFMAs on one
-    // accumulator from -m) interleaved with the probabilities of the current
-    // half (sc -> pb). Operand reads run three MFMAs ahead; the scheduling
-    // groups keep MFMA, read and softmax VALU interleaved.
-    auto phase_a = [&](int kb, int h, const f32x16& sc, f32x16& sn, bf16x8 (&pb)[2]) __attribute__((always_inline)) {
-      constexpr int PER = 8 / KS;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
-      uint32_t w[8];
+    // Phase A of a step: S(j+1) = K Q^T from the stage at kb (accumulators from
+    // -m) interleaved with the probabilities of S(j) (sc -> pb). Each group is
+    // one MFMA, the operand read three MFMAs ahead and one element pair of the
+    // softmax; an empty use at the group's end pins the pair's arithmetic
+    // between this MFMA and the next (the compiler would otherwise gather it
+    // after the last MFMA).
+    auto phase_a = [&](int kb, const f32x16 (&sc)[2], f32x16 (&sn)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+      constexpr int N = 2 * KS;
+      constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
+      uint32_t w[16];
       float ls[2] = {0.f, 0.f};
       bf16x8 kf[3];
 #pragma unroll
-      for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, h, i);
+      for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, i);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < KS; ++i) {
-        sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i], i == 0 ? mneg : sn, 0, 0, 0);
-        if (i + 3 < KS) kf[i % 3] = rdk(kb, h, i + 3);
+      for (int i = 0; i < N; ++i) {
+        sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? mneg : sn[i & 1], 0, 0, 0);
+        if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
           w[i * PER + u] = prob_pair(sc, i * PER + u, ls[(i * PER + u) & 1]);
-          // an empty use at the group's end places the pair's arithmetic
-          // between this MFMA and the next (the compiler would otherwise
-          // gather it after the last MFMA)
           asm volatile("" :: "v"(w[i * PER + u]));
         }
       }
       pack_pb(w, pb);
       l_run += ls[0] + ls[1];
     };
-    // Phase B of a sub-step: O^T += V^T P^T over the half's two 16-key slices
-    // (2 DT MFMAs) interleaved with the row maximum of sn (when given; already
-    // masked).
-    auto phase_b = [&](int vb, int h, const bf16x8 (&pb)[2], const f32x16* sn) __attribute__((always_inline)) -> float {
-      constexpr int N = 2 * DT;
-      constexpr int PER = 8 / N;    // max3 operations per MFMA
-      float x = -INFINITY;
+    // Probabilities of S alone (the last step of an entry).
+    auto probs_alone = [&](const f32x16 (&sc)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+      uint32_t w[16];
+      float ls[2] = {0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < 16; ++i) w[i] = prob_pair(sc, i, ls[i & 1]);
+      pack_pb(w, pb);
+      l_run += ls[0] + ls[1];
+    };
+    // Phase B of a step: O^T += V^T P^T from the stage at vb (operand reads
+    // three ahead), interleaved with the row maximum of sn when given (already
+    // masked); returns it relative to the base.
+    auto phase_b = [&](int vb, const bf16x8 (&pb)[4], const f32x16* sn) __attribute__((always_inline)) -> float {
+      constexpr int N = 4 * DT;
+      constexpr int PER = 16 / N;   // max3 operations per MFMA
+      float x[2] = {-INFINITY, -INFINITY};
       bf16x8 vf[3];
 #pragma unroll
-      for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, h, i);
+      for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, i);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < N; ++i) {
         oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pb[i / DT], oacc[i % DT], 0, 0, 0);
-        if (i + 3 < N) vf[i % 3] = rdv(vb, h, i + 3);
+        if (i + 3 < N) vf[i % 3] = rdv(vb, i + 3);
         if (sn) {
 #pragma unroll
           for (int u = 0; u < PER; ++u) {
-            const int e = 2 * (i * PER + u);
-            x = fmaxf(fmaxf(x, (*sn)[e]), (*sn)[e + 1]);
+            const int q = i * PER + u, h = q & 1, e = (q >> 1) * 2;
+            x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
+            asm volatile("" :: "v"(x[h]));
           }
-          asm volatile("" :: "v"(x));
         } else {
           __builtin_amdgcn_sched_barrier(0);
         }
       }
-      return sn ? max_pair32(x) : 0.f;
+      return sn ? max_pair32(fmaxf(x[0], x[1])) : 0.f;
     };
-    // Moves the base up by the half's maximum when it exceeds the base by kLazy.
-    auto rebase = [&](f32x16& sc) __attribute__((always_inline)) {
+    // Moves the base up by the step maximum when it exceeds the base by kLazy.
+    auto rebase = [&](f32x16 (&sc)[2]) __attribute__((always_inline)) {
       const bool grow = mx > kLazy;
       if (__builtin_amdgcn_ballot_w64(grow)) {
         const float delta = grow ? mx : 0.f;
         const float alpha = __builtin_amdgcn_exp2f(-delta);
-        sc -= delta;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) sc[h] -= delta;
         mneg -= delta;
         l_run *= alpha;
 #pragma unroll
@@ -691,60 +706,77 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       }
     };
     auto kbase = [&](int pp) { return (pp & (kStages - 1)) * KTILE; };
-    // keys of a half are all visible to every row of the entry
-    const int min_qpos = P + row0;
-    auto needs_mask = [&](int k0) { return k0 + 31 > min_qpos; };
+    auto vbase = [&](int pp) { return v_off + (pp & (kStages - 1)) * VTILE; };
+    // steps [0, n_full) are visible to every row of the entry (no mask)
+    const int n_full = max(0, min(nsteps, (P + row0 + 1) / kKv - kbeg));
 
-    // ---- S of the first half with the exact row maximum as base
-    f32x16 sa, sb;
-    qk_alone(kbase(p), 0, sa);
-    if (needs_mask(kbeg * kKv)) mask(sa, kbeg * kKv);
+    // ---- S(0) with the exact row maximum as base
+    f32x16 sa[2], sb[2];
+    qk_alone(kbase(p), sa);
+    if (n_full == 0) mask(sa, kbeg * kKv);
     {
-      // Finite when the run's first half has a visible key for this row (always
+      // Finite when the run's first step has a visible key for this row (always
       // so for the first run: key 0 is visible to every row). A row that sees no
-      // key of the run's first half sees none of its later keys either, so any
-      // base serves it.
+      // key of the run's first step sees none of its later steps either (they
+      // hold higher keys), so any base serves it.
       float m0 = rowmax(sa);
       if (m0 == -INFINITY) m0 = 0.f;
-      sa -= m0;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) sa[h] -= m0;
 #pragma unroll
       for (int e2 = 0; e2 < 16; ++e2) mneg[e2] = -m0;
     }
 
-    // Step j at ring position p: two halves. The current S (half 0 of step j)
-    // is in sa at the start; half 1's S goes to sb, the next step's half 0 back
-    // to sa.
-    auto step = [&](int j) __attribute__((always_inline)) {
-      const int st = p & (kStages - 1);
-      const int KB = st * KTILE, KB1 = ((st + 1) & (kStages - 1)) * KTILE, VB = v_off + st * VTILE;
-      const int k0 = (kbeg + j) * kKv;
+    // Step j < nsteps - 1 at ring position p: current S in sc, next S into sn.
+    auto step = [&](int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
       const bool direct = issue(p + kAhead);
-      bf16x8 pb[2];
-      // half 0: S(half 1 of step j) || P(half 0); PV(half 0) || max
-      rebase(sa);
-      phase_a(KB, 1, sa, sb, pb);
-      if (needs_mask(k0 + 32)) mask(sb, k0 + 32);
-      mx = phase_b(VB, 0, pb, &sb);
-      // half 1: S(half 0 of step j + 1) || P(half 1); PV(half 1) || max. On
-      // the entry's last step the next S is computed from whatever the next
-      // stage holds and discarded: the step stays one branch-free block
-      // instead of an arm without MFMAs for the last probabilities.
-      rebase(sb);
-      phase_a(KB1, 0, sb, sa, pb);
-      if (needs_mask(k0 + kKv)) mask(sa, k0 + kKv);
-      mx = phase_b(VB, 1, pb, &sa);
+      rebase(sc);
+      bf16x8 pb[4];
+      phase_a(kbase(p + 1), sc, sn, pb);
+      if (j + 1 >= n_full) mask(sn, (kbeg + j + 1) * kKv);
+      mx = phase_b(vbase(p), pb, sn);
       step_barrier(direct);
+      ++p;
     };
-    for (int j = 0; j < nsteps; ++j) {
-      if (j == nsteps - 1 && next_q) {   // the next entry's Q (qf stays in use)
-        if (row_ok_n) {
+    const int last = nsteps - 1;
+    // the next entry's Q, loaded into qn while qf is still in use (the last
+    // step of an entry computes no QK, so it is loaded before the step pair
+    // that ends the entry)
+    auto prefetch_q = [&]() __attribute__((always_inline)) {
+      if (!SPLIT) {
+        // qn is written on every path, so that it is not live across the
+        // steps of an entry
+        if (next_q && row_ok_n) {
           const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow_n * a.hq + head_n) * D);
 #pragma unroll
           for (int s = 0; s < KS; ++s) qn[s] = qp[2 * s + half];
+        } else {
+#pragma unroll
+          for (int s = 0; s < KS; ++s) qn[s] = u32x4{0, 0, 0, 0};
         }
-        q_ready = true;
+        q_ready = next_q;
       }
-      step(j);
+    };
+    int j = 0;
+    // two steps per iteration so the S buffers alternate without copies
+    for (; j + 1 < last; j += 2) {
+      step(j, sa, sb);
+      step(j + 1, sb, sa);
+    }
+    if (j < last) {
+      step(j, sa, sb);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) sa[h] = sb[h];
+      ++j;
+    }
+    prefetch_q();
+    {   // the entry's last step: P and PV only
+      const bool direct = issue(p + kAhead);
+      rebase(sa);
+      bf16x8 pb[4];
+      probs_alone(sa, pb);
+      phase_b(vbase(p), pb, nullptr);
+      step_barrier(direct);
       ++p;
     }
 
