@@ -238,6 +238,23 @@ __device__ __forceinline__ u32x4 load16_now(const void* src) {
   return v;
 }
 
+// Loads whose completion the compiler does not track. The attention kernel
+// mixes them with load-to-LDS copies it issues itself, which the compiler does
+// not see either; a load the compiler tracks makes it wait for every copy in
+// flight (vmcnt(0)) before the first use. The caller guarantees that a wait
+// covering the load (a step barrier's vmcnt) comes before the first read of the
+// result, and ties the read to that point with an empty asm statement.
+__device__ __forceinline__ int32_t load_word_untracked(const int32_t* src) {
+  int32_t v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(src));
+  return v;
+}
+__device__ __forceinline__ u32x4 load16_untracked(const void* src) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(src));
+  return v;
+}
+
 // One load-to-LDS copy: lane l's 16 bytes at base + off land at lds + 16 l.
 // base is wave-uniform (SGPRs), off a per-lane 32-bit offset; M0 holds the LDS
 // address (one wait state between writing M0 and the copy).
@@ -267,7 +284,9 @@ struct AttnGeom {
   static constexpr int BLK = D * 2 * kBs;       // one V^T block (D rows of 16 keys)
   static constexpr int VTILE = (kKv / kBs) * BLK;
   static constexpr int KREG = kStages * KTILE;  // the V stages start here
-  static constexpr int LDS = KREG + kStages * VTILE;
+  static constexpr int RING = KREG + kStages * VTILE;
+  static constexpr int STAGING = 4096;          // per-wave area after the ring
+  static constexpr int LDS = RING + kAttnWaves * STAGING;
   static constexpr int RPL = 1024 / RB;         // K rows per 1 KB copy
   static constexpr int LPW = kBs * RB / 1024;   // 1 KB copies per block and tensor
   static constexpr int KS = D / 16;             // MFMA k-steps over D
@@ -391,52 +410,91 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       if (ck < cend) return;
     }
   };
-  // Physical block of this wave's slot at the cursor's step, or -1 past the
-  // prompt / outside the pool; the table index is clamped into the row.
-  auto cursor_block = [&]() __attribute__((always_inline)) -> int {
-    const int nblk = (cL + kBs - 1) / kBs;
-    const int lb = ck * (kKv / kBs) + bs;
-    cint32_t* row = reinterpret_cast<cint32_t*>(reinterpret_cast<uintptr_t>(a.bt)) + int64_t(cr) * a.bt_stride;
-    const int b = row[min(lb, nblk - 1)];
-    return (lb < nblk && b >= 0 && b < a.num_blocks) ? b : -1;
+  // Block-table word of this wave's slot at the cursor's step, loaded one step
+  // before its copies: issue() loads it before its own copies, so the step
+  // barrier that follows (which leaves only those copies in flight) completes
+  // it. The index is clamped into the row; bin says whether it was inside the
+  // prompt. Past the last entry a harmless word (the plan's first) is loaded.
+  int32_t bword = 0;
+  bool bin = false;
+  auto cursor_load = [&]() __attribute__((always_inline)) {
+    const int32_t* w = reinterpret_cast<const int32_t*>(a.plan);
+    bin = false;
+    if (!cdone) {
+      const int nblk = (cL + kBs - 1) / kBs;
+      const int lb = ck * (kKv / kBs) + bs;
+      bin = lb < nblk;
+      w = a.bt + int64_t(cr) * a.bt_stride + min(lb, nblk - 1);
+    }
+    bword = load_word_untracked(w);
   };
   cursor_next_entry();
-  int bnext = cdone ? -1 : cursor_block();
-  // Copies the cursor's step into ring position p and advances the cursor.
-  // Returns whether load-to-LDS copies of this wave are in flight (a block that
-  // is not whole is written through registers and waited for at once).
-  auto issue = [&](int p) __attribute__((always_inline)) -> bool {
+  cursor_load();
+  // This wave's area after the ring (output staging; the target of copies
+  // that carry nothing).
+  const uint32_t own_area = lds0 + G::RING + wave * G::STAGING;
+  // The copies of a step are spread over the step's MFMAs rather than issued
+  // together: eight waves issuing all of theirs at once fill the load queue
+  // and stall at the step start. issue() records where copy k goes; a copy
+  // of a step without load-to-LDS copies rewrites this wave's own area with
+  // bytes of block 0, which nothing reads (the step then waits for all).
+  uint64_t cp_src = reinterpret_cast<uintptr_t>(cache);
+  uint32_t cp_dst = own_area, cp_stride = 0;
+  auto copy_part = [&](int k) __attribute__((always_inline)) {
+    copy16_to_lds(reinterpret_cast<const void*>(cp_src), src_off[k], cp_dst + k * cp_stride);
+  };
+  // Copies the cursor's step into ring position p (now, or through copy_part
+  // when `spread`) and advances the cursor. Returns whether load-to-LDS
+  // copies of this wave are in flight (a block that is not whole is written
+  // through registers and waited for at once). A wait that completes the
+  // table word loaded by the previous call comes first.
+  auto issue = [&](int p, bool spread) __attribute__((always_inline)) -> bool {
+    cp_src = reinterpret_cast<uintptr_t>(cache);
+    cp_dst = own_area;
+    cp_stride = 0;
     if (cdone) return false;
-    const int b = bnext;
+    int32_t word = bword;
+    asm volatile("" : "+v"(word));
+    const int raw = __builtin_amdgcn_readfirstlane(word);
+    // physical block, or -1 past the prompt / outside the pool
+    const int b = (bin && raw >= 0 && raw < a.num_blocks) ? raw : -1;
     const int key0 = ck * kKv + bs * kBs;
+    const int L = cL;
     const uint32_t dst = lds0 + (p & (kStages - 1)) * stage_stride + slot0;
     const uint8_t* src = cache + (int64_t(b < 0 ? 0 : b) * a.hkv + cg) * (kBs * RB);
+    if (++ck == cend) cursor_next_entry();
+    cursor_load();
     bool direct = false;
-    if (b >= 0 && key0 + kBs <= cL) {   // wave-uniform: the whole block is valid
+    if (b >= 0 && key0 + kBs <= L) {   // wave-uniform: the whole block is valid
+      if (spread) {
+        cp_src = reinterpret_cast<uintptr_t>(src);
+        cp_dst = dst;
+        cp_stride = 1024;
+      } else {
 #pragma unroll
-      for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
+        for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
+      }
       direct = true;
     } else {
       const u32x4 zero{0, 0, 0, 0};
 #pragma unroll
       for (int i = 0; i < LPW; ++i) {
-        u32x4 v = zero;
-        if (b >= 0) v = load16_now(src + src_off[i]);
+        // (a missing block loads block 0 and discards it, so that every path
+        // through here waits for the memory operations issued before it)
+        u32x4 v = load16_now(src + src_off[i]);
         if (is_v) {
           // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
           const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
-          const int vn = b < 0 ? 0 : min(8, max(0, cL - key0 - h8));
+          const int vn = b < 0 ? 0 : min(8, max(0, L - key0 - h8));
 #pragma unroll
           for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
         } else {
-          const bool ok = b >= 0 && key0 + RPL * i + lane / NC < cL;
+          const bool ok = b >= 0 && key0 + RPL * i + lane / NC < L;
           v = ok ? v : zero;
         }
         *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
       }
     }
-    if (++ck == cend) cursor_next_entry();
-    bnext = cdone ? -1 : cursor_block();
     return direct;
   };
   // End of a step: this wave's copies for the next steps have landed (the
@@ -470,25 +528,49 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lds + addr));
   };
 
-  // ---- first steps of the queue
-  int p = 0;   // ring position of the next step to compute
-  bool last_direct = false;
-#pragma unroll
-  for (int i = 0; i < kAhead; ++i) last_direct = issue(i);
-  (void)last_direct;
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-
-  // Q of the next entry, loaded (raw bf16) during the current entry's last
-  // step so that an entry starts without waiting for its queries.
-  u32x4 qn[KS];
-  bool q_ready = false;
   // This lane's query column inside a tile.
   const int m = wave * 32 + l32;
   const int hh = m / a.per_tile;
   const int pos = m - hh * a.per_tile;
+
+  // Raw Q (bf16) of the entry to come, loaded before the first steps for the
+  // first entry and during an entry's last step for the next one, so that an
+  // entry starts without waiting for its queries (unsplit kernel only).
+  u32x4 qn[KS];
+  // This lane's Q row in entry e; row 0 of Q for a lane without a row or past
+  // the last entry (the load stays inside Q and the entry discards the value).
+  auto q_source = [&](int e) __attribute__((always_inline)) -> const u32x4* {
+    int64_t off = 0;
+    if (e < a.num_entries) {
+      cint32_t* en = ents + int64_t(e) * kEntryWords;
+      const int r = en[cw::kEntR], nv = en[cw::kEntNvalid];
+      const int64_t row = int64_t(en[cw::kEntCu0]) + en[cw::kEntRow0] + pos;
+      const int hd = en[cw::kEntG] * a.group + hh;
+      off = (r >= 0 && hh < a.group && pos < nv) ? (row * a.hq + hd) * D : 0;
+    }
+    return reinterpret_cast<const u32x4*>(a.q + off);
+  };
+  auto load_q = [&](const u32x4* qp) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qn[s] = load16_untracked(qp + 2 * s + half);
+  };
+  if (!SPLIT) load_q(q_source(blockIdx.x));
+  // the first call below reads the table word loaded before the Q loads
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(SPLIT ? 0 : KS));
+
+  // ---- first steps of the queue
+  int p = 0;   // ring position of the next step to compute
+#pragma unroll
+  for (int i = 0; i < kAhead; ++i) {
+    // the next call reads the table word this one loaded: wait for it, leaving
+    // the copies issued after it in flight
+    if (issue(i, false)) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(LPW));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 
   for (int e = blockIdx.x; e < a.num_entries; e += grid) {
     cint32_t* en = ents + int64_t(e) * kEntryWords;
@@ -497,23 +579,9 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     for (int i = 0; i < cw::kEntFields; ++i) f[i] = en[i];
     // the end of the queue, or an entry that is not the one the planner wrote
     if (f[cw::kEntR] < 0 || uint32_t(en[cw::kEntCheck]) != cw::entry_check(a.fp_lo, a.fp_hi, f)) break;
-    // the next entry's rows, for the Q prefetch (valid: a whole entry with keys)
-    bool next_q = false;
-    int64_t qrow_n = 0;
-    int head_n = 0;
-    bool row_ok_n = false;
-    // (not on the split path, whose kernel has no registers to spare for it)
-    if (!SPLIT && e + grid < a.num_entries) {
-      cint32_t* nx = ents + int64_t(e + grid) * kEntryWords;
-      int32_t fn[cw::kEntFields];
-#pragma unroll
-      for (int i = 0; i < cw::kEntFields; ++i) fn[i] = nx[i];
-      next_q = fn[cw::kEntR] >= 0 && fn[cw::kEntKend] > fn[cw::kEntKbeg] &&
-               uint32_t(nx[cw::kEntCheck]) == cw::entry_check(a.fp_lo, a.fp_hi, fn);
-      row_ok_n = (hh < a.group) && (pos < fn[cw::kEntNvalid]);
-      qrow_n = int64_t(fn[cw::kEntCu0]) + fn[cw::kEntRow0] + pos;
-      head_n = fn[cw::kEntG] * a.group + hh;
-    }
+    // where the next entry's Q comes from (the split kernel has no registers
+    // to spare for a prefetch)
+    const u32x4* q_next = SPLIT ? nullptr : q_source(e + grid);
     const int g = f[cw::kEntG], row0 = f[cw::kEntRow0], nvalid = f[cw::kEntNvalid];
     const int cu0 = f[cw::kEntCu0], P = f[cw::kEntP];
     const int kbeg = f[cw::kEntKbeg], kend = f[cw::kEntKend];
@@ -550,15 +618,12 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
       }
     } else {
-      if (!q_ready && row_ok) {
-        const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow * a.hq + head) * D);
+      // qn landed before the last step barrier (or the first steps' wait)
 #pragma unroll
-        for (int s = 0; s < KS; ++s) qn[s] = qp[2 * s + half];
-      }
+      for (int s = 0; s < KS; ++s) asm volatile("" : "+v"(qn[s]));
 #pragma unroll
       for (int s = 0; s < KS; ++s)
         qf[s] = row_ok ? scale_bf16x8(qn[s], a.c_log2) : __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
-      q_ready = false;
     }
 
     // Causal mask of the step starting at key k0: element e of accumulator h
@@ -632,6 +697,22 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // softmax; an empty use at the group's end pins the pair's arithmetic
     // between this MFMA and the next (the compiler would otherwise gather it
     // after the last MFMA).
+    // Where a step's copies go: the first half after MFMAs 0, E, 2E, .. of
+    // phase A, the second half likewise in phase B; a step without phase A
+    // (an entry's last) puts all of them in phase B.
+    constexpr int HALF_C = LPW / 2;
+    auto copies_a = [&](int i) __attribute__((always_inline)) {
+      constexpr int E = 2 * KS / HALF_C;
+      if (i % E == 0) copy_part(i / E);
+    };
+    auto copies_b = [&](int i, bool all) __attribute__((always_inline)) {
+      constexpr int E = 4 * DT / HALF_C, EA = 4 * DT / LPW;
+      if (all) {
+        if (i % EA == 0) copy_part(i / EA);
+      } else if (i % E == 0) {
+        copy_part(HALF_C + i / E);
+      }
+    };
     auto phase_a = [&](int kb, const f32x16 (&sc)[2], f32x16 (&sn)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
       constexpr int N = 2 * KS;
       constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
@@ -645,6 +726,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       for (int i = 0; i < N; ++i) {
         sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? mneg : sn[i & 1], 0, 0, 0);
         if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
+        copies_a(i);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
           w[i * PER + u] = prob_pair(sc, i * PER + u, ls[(i * PER + u) & 1]);
@@ -678,6 +760,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       for (int i = 0; i < N; ++i) {
         oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pb[i / DT], oacc[i % DT], 0, 0, 0);
         if (i + 3 < N) vf[i % 3] = rdv(vb, i + 3);
+        copies_b(i, sn == nullptr);
         if (sn) {
 #pragma unroll
           for (int u = 0; u < PER; ++u) {
@@ -729,7 +812,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 
     // Step j < nsteps - 1 at ring position p: current S in sc, next S into sn.
     auto step = [&](int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
-      const bool direct = issue(p + kAhead);
+      const bool direct = issue(p + kAhead, true);
       rebase(sc);
       bf16x8 pb[4];
       phase_a(kbase(p + 1), sc, sn, pb);
@@ -739,24 +822,6 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       ++p;
     };
     const int last = nsteps - 1;
-    // the next entry's Q, loaded into qn while qf is still in use (the last
-    // step of an entry computes no QK, so it is loaded before the step pair
-    // that ends the entry)
-    auto prefetch_q = [&]() __attribute__((always_inline)) {
-      if (!SPLIT) {
-        // qn is written on every path, so that it is not live across the
-        // steps of an entry
-        if (next_q && row_ok_n) {
-          const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow_n * a.hq + head_n) * D);
-#pragma unroll
-          for (int s = 0; s < KS; ++s) qn[s] = qp[2 * s + half];
-        } else {
-#pragma unroll
-          for (int s = 0; s < KS; ++s) qn[s] = u32x4{0, 0, 0, 0};
-        }
-        q_ready = next_q;
-      }
-    };
     int j = 0;
     // two steps per iteration so the S buffers alternate without copies
     for (; j + 1 < last; j += 2) {
@@ -769,9 +834,11 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       for (int h = 0; h < 2; ++h) sa[h] = sb[h];
       ++j;
     }
-    prefetch_q();
-    {   // the entry's last step: P and PV only
-      const bool direct = issue(p + kAhead);
+    {   // the entry's last step: P and PV only. qf is no longer needed: the
+        // next entry's Q is loaded now, ahead of this step's table word and
+        // copies, so that this step's barrier completes it.
+      if (!SPLIT) load_q(q_next);
+      const bool direct = issue(p + kAhead, true);
       rebase(sa);
       bf16x8 pb[4];
       probs_alone(sa, pb);
@@ -781,8 +848,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     }
 
     const float l_tot = sum_pair32(l_run);
-    if (!row_ok) continue;
     if constexpr (SPLIT) {
+      if (!row_ok) continue;
       const int64_t prow = int64_t(split) * a.part_rows + qrow * a.hq + head;
       float* po = a.part_o + prow * D;
       const bool any = l_tot > 0.f;
@@ -797,17 +864,39 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       // base-2 log-sum-exp of the scaled scores: the base plus log2 of the sum
       if (half == 0) a.part_lse[prow] = any ? -mneg[0] + __log2f(l_tot) : -INFINITY;
     } else {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + (qrow * a.hq + head) * D;
+      // The output goes through this wave's staging area: a lane holds 4
+      // consecutive d of its row per (t, gq), so direct stores would write 32
+      // rows in 8-byte pieces per instruction. Rows are staged (16-byte chunks
+      // swizzled like K rows) and read back NC lanes per row, so that each
+      // store covers whole rows.
+      constexpr int SROWS = G::STAGING / RB;   // rows staged per round
+      constexpr int RPI = 64 / NC;             // rows per read-back instruction
+      const float inv = row_ok ? 1.f / l_tot : 0.f;
+      // this lane's output row (suffix row x Hq + head), -1 for none
+      const int orow = row_ok ? int(qrow * a.hq + head) : -1;
+      uint8_t* stg = lds + G::RING + wave * G::STAGING;
 #pragma unroll
-      for (int t = 0; t < DT; ++t)
+      for (int rd = 0; rd < 32 / SROWS; ++rd) {
+        if (l32 / SROWS == rd) {
+          const int r = l32 % SROWS;
 #pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-          const int d = t * 32 + gq * 8 + half * 4;
-          const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
-                        pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
-          *reinterpret_cast<u32x2*>(op + d) = w;
+          for (int t = 0; t < DT; ++t)
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+              const int c = t * 4 + gq;   // 16-byte chunk: d = 8 c .. 8 c + 7
+              const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
+                            pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
+              *reinterpret_cast<u32x2*>(stg + r * RB + ((c ^ G::kswz(r)) << 4) + half * 8) = w;
+            }
         }
+#pragma unroll
+        for (int q = 0; q < SROWS / RPI; ++q) {
+          const int r = q * RPI + lane / NC, c = lane % NC;
+          const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * RB + ((c ^ G::kswz(r)) << 4));
+          const int ro = __shfl(orow, rd * SROWS + r);
+          if (ro >= 0) *reinterpret_cast<u32x4*>(a.out + int64_t(ro) * D + c * 8) = v;
+        }
+      }
     }
   }
   // Every copy the cursor issued was consumed: the cursor runs out with the
