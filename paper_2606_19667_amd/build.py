@@ -13,6 +13,11 @@ import subprocess
 import sys
 import tempfile
 
+try:
+    from . import asm_check
+except ImportError:   # run as a script
+    import asm_check
+
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
@@ -69,6 +74,15 @@ def build(verbose: bool = False) -> str:
             objs.append(obj)
             if verbose and out:
                 print(out)
+        # The attention kernel's untracked loads are checked on its assembly
+        # (asm_check): no path may touch their registers before a covering wait.
+        asm = os.path.join(tmp, "cw_kernels.s")
+        _run([HIPCC, *HIP_FLAGS, *EXTRA_FLAGS["cw_kernels.hip"], *incs, "--cuda-device-only", "-S",
+              os.path.join(CSRC, "cw_kernels.hip"), "-o", asm])
+        with open(asm) as fh:
+            report = asm_check.check(fh.read())
+        if verbose:
+            print("untracked loads checked:", report)
         tmp_lib = os.path.join(tmp, "libcw.so")
         _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp_lib])
         shutil.move(tmp_lib, LIB)

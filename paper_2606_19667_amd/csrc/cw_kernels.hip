@@ -453,9 +453,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     cp_dst = own_area;
     cp_stride = 0;
     if (cdone) return false;
-    int32_t word = bword;
-    asm volatile("" : "+v"(word));
-    const int raw = __builtin_amdgcn_readfirstlane(word);
+    asm volatile("" : "+v"(bword));
+    const int raw = __builtin_amdgcn_readfirstlane(bword);
     // physical block, or -1 past the prompt / outside the pool
     const int b = (bin && raw >= 0 && raw < a.num_blocks) ? raw : -1;
     const int key0 = ck * kKv + bs * kBs;
@@ -537,15 +536,28 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // first entry and during an entry's last step for the next one, so that an
   // entry starts without waiting for its queries (unsplit kernel only).
   u32x4 qn[KS];
-  // This lane's Q row in entry e; row 0 of Q for a lane without a row or past
-  // the last entry (the load stays inside Q and the entry discards the value).
-  auto q_source = [&](int e) __attribute__((always_inline)) -> const u32x4* {
+  // Plan entry words of the entry to come and of the one after it, one word
+  // per lane: lane l holds word l % 16 of entry e (l % 32 < 16) or of entry
+  // e + grid (l % 32 >= 16; past the last entry, the last entry's words).
+  // Loaded with the queries, so that an entry starts without a scalar load.
+  int32_t desc = 0;
+  auto load_desc = [&](int e) __attribute__((always_inline)) {
+    const int idx = min(e + ((lane >> 4) & 1) * grid, a.num_entries - 1);
+    desc = load_word_untracked(a.plan + kPlanHeader + int64_t(idx) * kEntryWords + (lane & 15));
+  };
+  // word i of the entry (second = false) or of the one after it
+  auto desc_word = [&](int32_t dw, bool second, int i) __attribute__((always_inline)) -> int {
+    return __builtin_amdgcn_readlane(dw, (second ? 16 : 0) + i);
+  };
+  // This lane's Q row in the entry after the current one (`exists` false past
+  // the last entry); row 0 of Q for a lane without a row or past the last
+  // entry (the load stays inside Q and the entry discards the value).
+  auto q_source = [&](int32_t dw, bool second, bool exists) __attribute__((always_inline)) -> const u32x4* {
     int64_t off = 0;
-    if (e < a.num_entries) {
-      cint32_t* en = ents + int64_t(e) * kEntryWords;
-      const int r = en[cw::kEntR], nv = en[cw::kEntNvalid];
-      const int64_t row = int64_t(en[cw::kEntCu0]) + en[cw::kEntRow0] + pos;
-      const int hd = en[cw::kEntG] * a.group + hh;
+    if (exists) {
+      const int r = desc_word(dw, second, cw::kEntR), nv = desc_word(dw, second, cw::kEntNvalid);
+      const int64_t row = int64_t(desc_word(dw, second, cw::kEntCu0)) + desc_word(dw, second, cw::kEntRow0) + pos;
+      const int hd = desc_word(dw, second, cw::kEntG) * a.group + hh;
       off = (r >= 0 && hh < a.group && pos < nv) ? (row * a.hq + hd) * D : 0;
     }
     return reinterpret_cast<const u32x4*>(a.q + off);
@@ -554,9 +566,12 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
     for (int s = 0; s < KS; ++s) qn[s] = load16_untracked(qp + 2 * s + half);
   };
-  if (!SPLIT) load_q(q_source(blockIdx.x));
-  // the first call below reads the table word loaded before the Q loads
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(SPLIT ? 0 : KS));
+  load_desc(blockIdx.x);
+  // the wait that completes the words (and the table word loaded before),
+  // tied to the register that receives them
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(desc) :: "memory");
+  if (!SPLIT) load_q(q_source(desc, false, true));
+  // the first call below reads the table word: complete since the wait above
 
   // ---- first steps of the queue
   int p = 0;   // ring position of the next step to compute
@@ -573,15 +588,19 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   asm volatile("" ::: "memory");
 
   for (int e = blockIdx.x; e < a.num_entries; e += grid) {
-    cint32_t* en = ents + int64_t(e) * kEntryWords;
+    // the words landed before the previous entry's last step barrier (or the
+    // first steps' wait)
+    asm volatile("" : "+v"(desc));
+    const int32_t dw = desc;
     int32_t f[cw::kEntFields];
 #pragma unroll
-    for (int i = 0; i < cw::kEntFields; ++i) f[i] = en[i];
+    for (int i = 0; i < cw::kEntFields; ++i) f[i] = desc_word(dw, false, i);
     // the end of the queue, or an entry that is not the one the planner wrote
-    if (f[cw::kEntR] < 0 || uint32_t(en[cw::kEntCheck]) != cw::entry_check(a.fp_lo, a.fp_hi, f)) break;
+    if (f[cw::kEntR] < 0 || uint32_t(desc_word(dw, false, cw::kEntCheck)) != cw::entry_check(a.fp_lo, a.fp_hi, f))
+      break;
     // where the next entry's Q comes from (the split kernel has no registers
     // to spare for a prefetch)
-    const u32x4* q_next = SPLIT ? nullptr : q_source(e + grid);
+    const u32x4* q_next = SPLIT ? nullptr : q_source(dw, true, e + grid < a.num_entries);
     const int g = f[cw::kEntG], row0 = f[cw::kEntRow0], nvalid = f[cw::kEntNvalid];
     const int cu0 = f[cw::kEntCu0], P = f[cw::kEntP];
     const int kbeg = f[cw::kEntKbeg], kend = f[cw::kEntKend];
@@ -604,6 +623,9 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
             *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
         if (half == 0) a.part_lse[prow] = -INFINITY;
       }
+      // the next entry's words, waited for here (this entry has no last step)
+      load_desc(e + grid);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       continue;
     }
 
@@ -736,19 +758,46 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       pack_pb(w, pb);
       l_run += ls[0] + ls[1];
     };
-    // Probabilities of S alone (the last step of an entry).
-    auto probs_alone = [&](const f32x16 (&sc)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+    // The last step of an entry (no next scores): O^T += V^T P^T with the
+    // probabilities of 16-key slice kk + 1 formed while the PV MFMAs of slice
+    // kk run (slice 0 first, alone); all of the step's copies go here.
+    auto phase_last = [&](int vb, const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+      constexpr int N = 4 * DT;
+      constexpr int PER = 4 / DT;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
       uint32_t w[16];
       float ls[2] = {0.f, 0.f};
+      bf16x8 vf[3];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) w[i] = prob_pair(sc, i, ls[i & 1]);
-      pack_pb(w, pb);
+      for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, i);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = prob_pair(sc, i, ls[i & 1]);
+      bf16x8 pk = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int kk = i / DT;
+        oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pk, oacc[i % DT], 0, 0, 0);
+        if (i + 3 < N) vf[i % 3] = rdv(vb, i + 3);
+        copies_b(i, true);
+        if (kk + 1 < 4) {
+#pragma unroll
+          for (int u = 0; u < PER; ++u) {
+            const int q = (kk + 1) * 4 + (i % DT) * PER + u;
+            w[q] = prob_pair(sc, q, ls[q & 1]);
+            asm volatile("" :: "v"(w[q]));
+          }
+        } else {
+          asm volatile("" :: "v"(vf[(i + 1) % 3]));
+        }
+        if (i % DT == DT - 1 && kk + 1 < 4)
+          pk = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk + 4], w[4 * kk + 5], w[4 * kk + 6], w[4 * kk + 7]});
+      }
       l_run += ls[0] + ls[1];
     };
     // Phase B of a step: O^T += V^T P^T from the stage at vb (operand reads
-    // three ahead), interleaved with the row maximum of sn when given (already
-    // masked); returns it relative to the base.
-    auto phase_b = [&](int vb, const bf16x8 (&pb)[4], const f32x16* sn) __attribute__((always_inline)) -> float {
+    // three ahead), interleaved with the row maximum of the next scores sn
+    // (already masked); returns it relative to the base.
+    auto phase_b = [&](int vb, const bf16x8 (&pb)[4], const f32x16 (&sn)[2]) __attribute__((always_inline)) -> float {
       constexpr int N = 4 * DT;
       constexpr int PER = 16 / N;   // max3 operations per MFMA
       float x[2] = {-INFINITY, -INFINITY};
@@ -760,19 +809,15 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       for (int i = 0; i < N; ++i) {
         oacc[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pb[i / DT], oacc[i % DT], 0, 0, 0);
         if (i + 3 < N) vf[i % 3] = rdv(vb, i + 3);
-        copies_b(i, sn == nullptr);
-        if (sn) {
+        copies_b(i, false);
 #pragma unroll
-          for (int u = 0; u < PER; ++u) {
-            const int q = i * PER + u, h = q & 1, e = (q >> 1) * 2;
-            x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
-            asm volatile("" :: "v"(x[h]));
-          }
-        } else {
-          __builtin_amdgcn_sched_barrier(0);
+        for (int u = 0; u < PER; ++u) {
+          const int q = i * PER + u, h = q & 1, e = (q >> 1) * 2;
+          x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
+          asm volatile("" :: "v"(x[h]));
         }
       }
-      return sn ? max_pair32(fmaxf(x[0], x[1])) : 0.f;
+      return max_pair32(fmaxf(x[0], x[1]));
     };
     // Moves the base up by the step maximum when it exceeds the base by kLazy.
     auto rebase = [&](f32x16 (&sc)[2]) __attribute__((always_inline)) {
@@ -838,11 +883,10 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         // next entry's Q is loaded now, ahead of this step's table word and
         // copies, so that this step's barrier completes it.
       if (!SPLIT) load_q(q_next);
+      load_desc(e + grid);
       const bool direct = issue(p + kAhead, true);
       rebase(sa);
-      bf16x8 pb[4];
-      probs_alone(sa, pb);
-      phase_b(vbase(p), pb, nullptr);
+      phase_last(vbase(p), sa);
       step_barrier(direct);
       ++p;
     }

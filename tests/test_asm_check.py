@@ -1,0 +1,56 @@
+"""The build's assembly check for untracked loads (paper_2606_19667_amd/asm_check.py)
+on hand-written gfx9 snippets."""
+import pytest
+
+from paper_2606_19667_amd import asm_check
+
+
+def _fn(body: str) -> str:
+    return "k:\n" + body + "\n\ts_endpgm\n.Lfunc_end0:\n"
+
+
+LOAD = "\t;;#ASMSTART\n\tglobal_load_dword v10, v[0:1], off\n\t;;#ASMEND\n"
+
+
+def _hazards(body):
+    return asm_check.hazards(_fn(body).split("\n"))
+
+
+def test_read_before_any_wait_is_reported():
+    assert _hazards(LOAD + "\tv_mov_b32_e32 v2, v10\n")
+
+
+def test_write_before_the_wait_is_reported():
+    assert _hazards(LOAD + "\tv_mov_b32_e32 v10, 0\n\ts_waitcnt vmcnt(0)\n")
+
+
+def test_wait_that_covers_the_load_clears_it():
+    body = LOAD + "".join(f"\tglobal_load_lds_dwordx4 v{20 + i}, s[4:5]\n" for i in range(4))
+    assert not _hazards(body + "\ts_waitcnt vmcnt(4)\n\tv_readfirstlane_b32 s6, v10\n")
+    # vmcnt(4) with only 3 younger memory instructions does not cover it
+    body3 = LOAD + "".join(f"\tglobal_load_lds_dwordx4 v{20 + i}, s[4:5]\n" for i in range(3))
+    assert _hazards(body3 + "\ts_waitcnt vmcnt(4)\n\tv_readfirstlane_b32 s6, v10\n")
+
+
+def test_every_path_is_followed():
+    body = LOAD + ("\ts_cbranch_scc1 .LBB0_2\n\ts_waitcnt vmcnt(0)\n.LBB0_2:\n"
+                   "\tv_readfirstlane_b32 s6, v10\n")
+    assert _hazards(body)
+    body_ok = LOAD + ("\ts_waitcnt vmcnt(0)\n\ts_cbranch_scc1 .LBB0_2\n\ts_nop 0\n.LBB0_2:\n"
+                      "\tv_readfirstlane_b32 s6, v10\n")
+    assert not _hazards(body_ok)
+
+
+def test_barrier_ends_the_window_and_waited_asm_loads_are_tracked():
+    assert not _hazards(LOAD + "\ts_barrier\n\tv_readfirstlane_b32 s6, v10\n")
+    waited = ("\t;;#ASMSTART\n\tglobal_load_dwordx4 v[10:13], v[0:1], off\n\ts_waitcnt vmcnt(0)\n"
+              "\t;;#ASMEND\n\tv_mov_b32_e32 v2, v10\n")
+    assert not _hazards(waited)
+
+
+def test_check_raises_with_the_function_name():
+    text = _fn(LOAD + "\tv_mov_b32_e32 v2, v10\n").replace("k:", "my_suffix_prefill_attn_kernel:")
+    with pytest.raises(RuntimeError, match="my_suffix_prefill_attn_kernel"):
+        asm_check.check(text)
+    with pytest.raises(RuntimeError, match="no function"):
+        asm_check.check(_fn("\ts_nop 0\n"))
