@@ -237,6 +237,40 @@ def question_only_point(seed: int, stream):
     return res
 
 
+def config_points(seed: int, stream, names=("llama8b-single", "topk10-f0.6", "llama70b-long-high")) -> dict:
+    """Attention time of the other configurations (not the headline): the
+    single 8B-shaped request, the top-k sweep at 60 % cached blocks and the
+    70B-shaped long-context batch in trie order (high hit). Each batch is
+    materialised on the GPU, its suffix appended, then the attention call is
+    timed with HIP events (median of several calls after a warm-up)."""
+    import torch
+    from paper_2606_19667_amd import batch as B
+    from paper_2606_19667_amd import cw
+    out_all = {}
+    for name in names:
+        w = make_workload(name, seed)
+        db = B.materialize(w, device="cuda", keep_host=[], gen_device="cuda")
+        cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
+        out = torch.empty_like(db.q)
+        S = np.diff(db.sched.cu_suffix)
+        P = db.sched.prefix_len
+        hq, hkv, D = w.num_q_heads, w.num_kv_heads, w.head_dim
+        fl = attention_flops(P, S, hq, D)
+        fn = lambda: cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale, out=out, stream=stream)
+        n = max(3, min(50, int(2e12 / fl)))
+        for _ in range(max(2, n // 5)):
+            fn()
+        t = percentiles_us(timed_calls(fn, stream, n))
+        sec = t["median"] * 1e-6
+        out_all[name] = {"attention_us": t, "GFLOP": round(fl / 1e9, 3),
+                         "achieved_TFLOPs": round(fl / sec / 1e12, 2),
+                         "frac": round(fl / sec / 1e12 / PEAK_BF16_TFLOPS, 4),
+                         "batch": int(S.size), "suffix_tokens": int(S.sum()), "prefix_tokens": int(P.sum())}
+        del db, out
+        torch.cuda.empty_cache()
+    return out_all
+
+
 def mfma_peak_point(seed: int, stream, workgroups: int = 1024, iters: int = 2000) -> dict:
     """The bf16 MFMA rate this card sustains (cw_probe_mfma_bf16: 8 independent
     32x32x16 accumulators per wave, two waves per SIMD, no memory traffic), on
@@ -556,6 +590,9 @@ def main() -> int:
         print("[bench] question-only diagnostic point", file=sys.stderr, flush=True)
         res["diagnostic_question_only"] = question_only_point(args.seed, stream)
         torch.cuda.empty_cache()
+    if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
+        print("[bench] other configurations (attention only)", file=sys.stderr, flush=True)
+        res["configs"] = config_points(args.seed, stream)
     if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
         print("[bench] suffix QKV projection + rotary embedding + append", file=sys.stderr, flush=True)
         res["qkv_projection"] = qkv_projection_point(w, args.seed, stream)

@@ -1,6 +1,6 @@
 """Builds libcw.so in-tree for gfx950.
 
-    python -m paper_2606_19667_amd.build
+    python -m paper_2606_19667_amd.build [-v] [--sanitize]
 
 The host sources build with g++, the HIP sources with hipcc for gfx950; hipcc
 links the shared library against the HIP runtime.
@@ -56,14 +56,25 @@ def _run(cmd):
     return proc.stdout
 
 
-def build(verbose: bool = False) -> str:
-    """Compiles every source and links libcw.so; returns its path."""
+# Host sources built with AddressSanitizer and UndefinedBehaviorSanitizer
+# (`--sanitize`): the library is linked by g++ into libcw_sanitized.so, which
+# cw.py loads when CW_LIBRARY names it (the process preloads libasan/libubsan).
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=undefined"]
+LIB_SANITIZED = os.path.join(PKG, "libcw_sanitized.so")
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compiles every source and links libcw.so (libcw_sanitized.so with
+    `sanitize`); returns its path."""
     incs = [f"-I{INCLUDE}", f"-I{CSRC}"]
+    gxx = shutil.which("g++") or "g++"
+    host_flags = HOST_FLAGS + (SANITIZE_FLAGS if sanitize else [])
     with tempfile.TemporaryDirectory(prefix="cw_build_") as tmp:
         objs = []
         for src in HOST_SOURCES:
             obj = os.path.join(tmp, src + ".o")
-            out = _run([shutil.which("g++") or "g++", *HOST_FLAGS, *incs, "-c",
+            out = _run([gxx, *host_flags, *incs, "-c",
                         os.path.join(CSRC, src), "-o", obj])
             objs.append(obj)
             if verbose and out:
@@ -84,10 +95,16 @@ def build(verbose: bool = False) -> str:
         if verbose:
             print("untracked loads checked:", report)
         tmp_lib = os.path.join(tmp, "libcw.so")
+        if sanitize:
+            rocm_lib = os.path.join(ROCM, "lib")
+            _run([gxx, "-shared", "-fPIC", "-fsanitize=address,undefined", *objs, f"-L{rocm_lib}",
+                  "-lamdhip64", f"-Wl,-rpath,{rocm_lib}", "-o", tmp_lib])
+            shutil.move(tmp_lib, LIB_SANITIZED)
+            return LIB_SANITIZED
         _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp_lib])
         shutil.move(tmp_lib, LIB)
     return LIB
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv))

@@ -17,7 +17,8 @@ import os
 import numpy as np
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcw.so")
+# CW_LIBRARY may name another build of the same library (the sanitizer build)
+LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcw.so")
 
 CW_OK = 0
 CW_EINVAL = -1
