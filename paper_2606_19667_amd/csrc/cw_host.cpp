@@ -617,7 +617,9 @@ std::vector<Entry> plan_entries(const int32_t* cu, const int32_t* plen, int32_t 
         for (int32_t s = 0; s < splits; ++s) {
           Entry e;
           const int32_t kb = std::min(n, s * run), ke = std::min(n, kb + run);
-          const int32_t f[cw::kEntFields] = {r, g, row0, nvalid, cu[r], P, P + S, kb, ke, s};
+          // steps whose keys every row of the entry sees (key 64 k + 63 <= P + row0)
+          const int32_t nfull = std::max(0, std::min(ke - kb, (P + row0 + 1) / cw::kKvTile - kb));
+          const int32_t f[cw::kEntFields] = {r, g, row0, nvalid, cu[r], P, P + S, kb, ke, s, nfull, cu[r] + row0};
           std::copy(f, f + cw::kEntFields, e.f);
           e.cost = (ke - kb) + (ke > kb ? kEntryOverhead : 0);
           e.pair = r * hkv + g;
@@ -781,7 +783,7 @@ extern "C" cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const
       } else {
         out[cw::kEntR] = -1;   // end of this queue
       }
-      out[cw::kEntCheck] = int32_t(cw::entry_check(lo, hi, out));
+      out[cw::kEntCheck] = int32_t(cw::entry_tag(lo, hi, uint32_t(int64_t(i) * qs.grid + w)));
     }
   return cw::ok();
 }

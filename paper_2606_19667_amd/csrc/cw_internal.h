@@ -43,18 +43,20 @@ constexpr int kHdrMagic = 0, kHdrEntries = 1, kHdrFpLo = 2, kHdrFpHi = 3, kHdrGr
               kHdrWork = 12;
 // entry words: request (-1 ends a queue), KV head, first suffix row, rows,
 // the request's first row in q/out, its prefix and prompt lengths, the run of
-// 64-key steps [kbeg, kend), the run's index, and a check word
+// 64-key steps [kbeg, kend), the run's index, the number of the run's steps
+// (from kbeg) that every row sees whole (no causal mask), the entry's first
+// row in q/out, and a check word
 constexpr int kEntR = 0, kEntG = 1, kEntRow0 = 2, kEntNvalid = 3, kEntCu0 = 4, kEntP = 5, kEntL = 6,
-              kEntKbeg = 7, kEntKend = 8, kEntSplit = 9, kEntCheck = 15;
-constexpr int kEntFields = 10;   // words covered by the check word
+              kEntKbeg = 7, kEntKend = 8, kEntSplit = 9, kEntNfull = 10, kEntQrow = 11, kEntCheck = 15;
+constexpr int kEntFields = 12;   // words the planner fills besides the check word
 
-// Check word of a plan entry: a multiplicative hash of its fields seeded with
-// the batch fingerprint (the kernels recompute it; an entry that does not
-// match ends the queue).
-__host__ __device__ inline uint32_t entry_check(uint32_t fp_lo, uint32_t fp_hi, const int32_t* f) {
-  uint32_t h = fp_lo ^ (fp_hi * 0x9E3779B1u);
-  for (int i = 0; i < kEntFields; ++i) h = (h ^ uint32_t(f[i])) * 0x01000193u;
-  return h ^ (h >> 15);
+// Check word of the plan entry at position `index` of a plan body: derived
+// from the batch fingerprint and the position. The planner is deterministic,
+// so an entry whose word matches was written, at that position, by a plan for
+// this batch; the kernels end a queue at an entry that does not match (e.g.
+// entries of an earlier plan left behind a newer header in device memory).
+__host__ __device__ inline uint32_t entry_tag(uint32_t fp_lo, uint32_t fp_hi, uint32_t index) {
+  return (fp_lo ^ (index * 0x9E3779B1u)) + fp_hi;
 }
 
 // 64-bit fingerprint of a batch description as a plan is built for it.

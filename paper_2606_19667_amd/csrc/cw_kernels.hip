@@ -255,6 +255,24 @@ __device__ __forceinline__ u32x4 load16_untracked(const void* src) {
   return v;
 }
 
+// A word at a wave-uniform address (SGPRs), completion untracked as above.
+__device__ __forceinline__ int32_t load_word_untracked_s(const int32_t* base) {
+  const uint64_t b = reinterpret_cast<uintptr_t>(base);
+  const uint64_t bu = (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b >> 32)))) << 32) |
+                      uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b))));
+  int32_t v;
+  asm volatile("global_load_dword %0, %1, %2" : "=v"(v) : "v"(0u), "s"(bu));
+  return v;
+}
+
+// Brings the 128-byte line holding src (per lane) into L2 with a 4-byte
+// load-to-LDS per lane into lds_addr + 4 l, an area whose bytes nothing reads;
+// completion untracked as above.
+__device__ __forceinline__ void touch_line(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
+}
+
 // One load-to-LDS copy: lane l's 16 bytes at base + off land at lds + 16 l.
 // base is wave-uniform (SGPRs), off a per-lane 32-bit offset; M0 holds the LDS
 // address (one wait state between writing M0 and the copy).
@@ -359,8 +377,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   cint32_t* plan = reinterpret_cast<cint32_t*>(reinterpret_cast<uintptr_t>(a.plan));
   // A plan whose header does not carry the fingerprint of the batch the host
   // validated is not this batch's plan: compute nothing.
-  if (uint32_t(plan[2]) != a.fp_lo || uint32_t(plan[3]) != a.fp_hi) return;
-  cint32_t* ents = plan + kPlanHeader;
+  if (uint32_t(plan[cw::kHdrFpLo]) != a.fp_lo || uint32_t(plan[cw::kHdrFpHi]) != a.fp_hi) return;
+  const int32_t* const ents = a.plan + kPlanHeader;
   const int grid = int(gridDim.x);
 
   const int tid = threadIdx.x;
@@ -373,6 +391,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   const int bs = wave >> 1;
   const bool is_v = (wave & 1) != 0;
   const uint8_t* const cache = reinterpret_cast<const uint8_t*>(is_v ? a.vc : a.kc);
+  // bytes from one physical block of a tensor to the next
+  const int64_t blk_bytes = int64_t(a.hkv) * (kBs * RB);
   // Per-lane source offset inside a block and LDS destination of copy i
   // (relative to the wave's block slot in a stage; lane l lands at +16 l).
   uint32_t src_off[LPW];
@@ -386,58 +406,79 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       src_off[i] = row * RB + (((lane % NC) ^ G::kswz(row)) << 4);
     }
   }
-  const int slot0 = is_v ? KREG + bs * BLK : bs * kBs * RB;   // in stage 0
-  const int stage_stride = is_v ? VTILE : KTILE;
-
-  // ---- copy cursor: the entry and step whose blocks this wave copies next
-  int ce = blockIdx.x - grid;   // entry index
-  int cr = 0, cg = 0, cL = 0, ck = 0, cend = 0;
-  bool cdone = false;
-  auto cursor_next_entry = [&]() __attribute__((always_inline)) {
-    for (;;) {
-      ce += grid;
-      if (ce >= a.num_entries) { cdone = true; return; }
-      cint32_t* en = ents + int64_t(ce) * kEntryWords;
-      int32_t f[cw::kEntFields];
-#pragma unroll
-      for (int i = 0; i < cw::kEntFields; ++i) f[i] = en[i];
-      cr = f[cw::kEntR];
-      if (cr < 0 || uint32_t(en[cw::kEntCheck]) != cw::entry_check(a.fp_lo, a.fp_hi, f)) { cdone = true; return; }
-      cg = f[cw::kEntG];
-      cL = f[cw::kEntL];
-      ck = f[cw::kEntKbeg];
-      cend = f[cw::kEntKend];
-      if (ck < cend) return;
-    }
-  };
-  // Block-table word of this wave's slot at the cursor's step, loaded one step
-  // before its copies: issue() loads it before its own copies, so the step
-  // barrier that follows (which leaves only those copies in flight) completes
-  // it. The index is clamped into the row; bin says whether it was inside the
-  // prompt. Past the last entry a harmless word (the plan's first) is loaded.
-  int32_t bword = 0;
-  bool bin = false;
-  auto cursor_load = [&]() __attribute__((always_inline)) {
-    const int32_t* w = reinterpret_cast<const int32_t*>(a.plan);
-    bin = false;
-    if (!cdone) {
-      const int nblk = (cL + kBs - 1) / kBs;
-      const int lb = ck * (kKv / kBs) + bs;
-      bin = lb < nblk;
-      w = a.bt + int64_t(cr) * a.bt_stride + min(lb, nblk - 1);
-    }
-    bword = load_word_untracked(w);
-  };
-  cursor_next_entry();
-  cursor_load();
-  // This wave's area after the ring (output staging; the target of copies
-  // that carry nothing).
+  // LDS address of this wave's block slot in ring position 0
+  const uint32_t slot0 = lds0 + (is_v ? KREG + bs * BLK : bs * kBs * RB);
+  const uint32_t stage_stride = is_v ? VTILE : KTILE;
+  // This wave's area after the ring: output staging, and the target of loads
+  // whose data nothing reads.
   const uint32_t own_area = lds0 + G::RING + wave * G::STAGING;
+
+  // ---- copy cursor: the entry and step whose blocks this wave copies next.
+  // Its state is wave-uniform. The words of the next entry the cursor enters
+  // are prefetched into cdesc (lane l holds word l % 16), loaded when the
+  // cursor enters the entry before it, so that a step that moves the cursor to
+  // a new entry waits for no load.
+  int ce = blockIdx.x;   // index of the entry whose words are in cdesc
+  int c_left = 0;        // steps of the cursor's entry not yet issued
+  int c_lb = 0;          // this wave's logical block at the cursor's step
+  int c_whole = 0;       // logical blocks below this hold 16 keys of the prompt
+  int c_last = 0;        // last logical block inside the prompt
+  int c_L = 0;           // prompt length of the cursor's request
+  const int32_t* c_row = a.bt;   // block-table row of the cursor's request
+  const uint8_t* c_src = cache;  // this wave's tensor at the cursor's KV head
+  bool cdone = false;
+  auto entry_word_addr = [&](int e) __attribute__((always_inline)) -> const int32_t* {
+    return ents + int64_t(min(e, a.num_entries - 1)) * kEntryWords + (lane & 15);
+  };
+  int32_t cdesc = load_word_untracked(entry_word_addr(ce));
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(cdesc) :: "memory");
+  // Makes the entry whose words are in cdesc the cursor's entry and loads the
+  // words of the one after it; ends the cursor at the end of the queue or at
+  // an entry not written for this batch.
+  auto cursor_take = [&]() __attribute__((always_inline)) {
+    if (ce >= a.num_entries) { cdone = true; return; }
+    const int r = __builtin_amdgcn_readlane(cdesc, cw::kEntR);
+    const uint32_t tag = uint32_t(__builtin_amdgcn_readlane(cdesc, cw::kEntCheck));
+    if (r < 0 || tag != cw::entry_tag(a.fp_lo, a.fp_hi, uint32_t(ce))) { cdone = true; return; }
+    const int kb = __builtin_amdgcn_readlane(cdesc, cw::kEntKbeg);
+    c_left = __builtin_amdgcn_readlane(cdesc, cw::kEntKend) - kb;
+    c_lb = kb * (kKv / kBs) + bs;
+    c_L = __builtin_amdgcn_readlane(cdesc, cw::kEntL);
+    c_whole = c_L / kBs;
+    c_last = (c_L + kBs - 1) / kBs - 1;
+    c_row = a.bt + int64_t(r) * a.bt_stride;
+    c_src = cache + int64_t(__builtin_amdgcn_readlane(cdesc, cw::kEntG)) * (kBs * RB);
+    ce += grid;
+    cdesc = load_word_untracked(entry_word_addr(ce));
+  };
+  // As cursor_take, skipping entries without steps (empty split runs): each
+  // further entry first waits for the words its predecessor loaded (so every
+  // path back to the reads passes that wait).
+  auto cursor_enter = [&]() __attribute__((always_inline)) {
+    cursor_take();
+    if (!cdone && c_left == 0) {
+      do {
+        asm volatile("s_waitcnt vmcnt(0)" : "+v"(cdesc) :: "memory");
+        cursor_take();
+      } while (!cdone && c_left == 0);
+    }
+  };
+  // Block-table word of this wave's block at the cursor's step, loaded one
+  // step before its copies: issue() loads it before its own copies, so the
+  // step barrier that follows (which leaves only those copies in flight)
+  // completes it. The index is clamped into the prompt. Past the last entry a
+  // harmless word (the plan's first) is loaded.
+  int32_t bword = 0;
+  auto cursor_load = [&]() __attribute__((always_inline)) {
+    bword = load_word_untracked_s(cdone ? a.plan : c_row + min(c_lb, c_last));
+  };
+  cursor_enter();
+  cursor_load();
   // The copies of a step are spread over the step's MFMAs rather than issued
   // together: eight waves issuing all of theirs at once fill the load queue
-  // and stall at the step start. issue() records where copy k goes; a copy
-  // of a step without load-to-LDS copies rewrites this wave's own area with
-  // bytes of block 0, which nothing reads (the step then waits for all).
+  // and stall at the step start. issue() records where copy k goes; a copy of
+  // a step without load-to-LDS copies rewrites this wave's own area with bytes
+  // of block 0, which nothing reads (the step then waits for all).
   uint64_t cp_src = reinterpret_cast<uintptr_t>(cache);
   uint32_t cp_dst = own_area, cp_stride = 0;
   auto copy_part = [&](int k) __attribute__((always_inline)) {
@@ -446,8 +487,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // Copies the cursor's step into ring position p (now, or through copy_part
   // when `spread`) and advances the cursor. Returns whether load-to-LDS
   // copies of this wave are in flight (a block that is not whole is written
-  // through registers and waited for at once). A wait that completes the
-  // table word loaded by the previous call comes first.
+  // through registers and waited for at once). The table word it reads was
+  // completed by the wait before this call.
   auto issue = [&](int p, bool spread) __attribute__((always_inline)) -> bool {
     cp_src = reinterpret_cast<uintptr_t>(cache);
     cp_dst = own_area;
@@ -455,16 +496,16 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     if (cdone) return false;
     asm volatile("" : "+v"(bword));
     const int raw = __builtin_amdgcn_readfirstlane(bword);
+    const int lb = c_lb, L = c_L;
     // physical block, or -1 past the prompt / outside the pool
-    const int b = (bin && raw >= 0 && raw < a.num_blocks) ? raw : -1;
-    const int key0 = ck * kKv + bs * kBs;
-    const int L = cL;
-    const uint32_t dst = lds0 + (p & (kStages - 1)) * stage_stride + slot0;
-    const uint8_t* src = cache + (int64_t(b < 0 ? 0 : b) * a.hkv + cg) * (kBs * RB);
-    if (++ck == cend) cursor_next_entry();
+    const int b = (lb <= c_last && uint32_t(raw) < uint32_t(a.num_blocks)) ? raw : -1;
+    const bool whole = b >= 0 && lb < c_whole;
+    const uint8_t* src = c_src + int64_t(b < 0 ? 0 : b) * blk_bytes;
+    const uint32_t dst = slot0 + uint32_t(p & (kStages - 1)) * stage_stride;
+    c_lb += kKv / kBs;
+    if (--c_left == 0) cursor_enter();
     cursor_load();
-    bool direct = false;
-    if (b >= 0 && key0 + kBs <= L) {   // wave-uniform: the whole block is valid
+    if (whole) {   // wave-uniform: the whole block is valid
       if (spread) {
         cp_src = reinterpret_cast<uintptr_t>(src);
         cp_dst = dst;
@@ -473,28 +514,28 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
       }
-      direct = true;
-    } else {
-      const u32x4 zero{0, 0, 0, 0};
-#pragma unroll
-      for (int i = 0; i < LPW; ++i) {
-        // (a missing block loads block 0 and discards it, so that every path
-        // through here waits for the memory operations issued before it)
-        u32x4 v = load16_now(src + src_off[i]);
-        if (is_v) {
-          // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
-          const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
-          const int vn = b < 0 ? 0 : min(8, max(0, L - key0 - h8));
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
-        } else {
-          const bool ok = b >= 0 && key0 + RPL * i + lane / NC < L;
-          v = ok ? v : zero;
-        }
-        *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
-      }
+      return true;
     }
-    return direct;
+    const int key0 = lb * kBs;
+    const u32x4 zero{0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      // (a missing block loads block 0 and discards it, so that every path
+      // through here waits for the memory operations issued before it)
+      u32x4 v = load16_now(src + src_off[i]);
+      if (is_v) {
+        // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
+        const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
+        const int vn = b < 0 ? 0 : min(8, max(0, L - key0 - h8));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
+      } else {
+        const bool ok = b >= 0 && key0 + RPL * i + lane / NC < L;
+        v = ok ? v : zero;
+      }
+      *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
+    }
+    return false;
   };
   // End of a step: this wave's copies for the next steps have landed (the
   // copies issued in this step may still be in flight when `keep` says that
@@ -527,7 +568,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lds + addr));
   };
 
-  // This lane's query column inside a tile.
+  // This lane's query column inside a tile: head hh of the group, position pos.
   const int m = wave * 32 + l32;
   const int hh = m / a.per_tile;
   const int pos = m - hh * a.per_tile;
@@ -543,7 +584,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   int32_t desc = 0;
   auto load_desc = [&](int e) __attribute__((always_inline)) {
     const int idx = min(e + ((lane >> 4) & 1) * grid, a.num_entries - 1);
-    desc = load_word_untracked(a.plan + kPlanHeader + int64_t(idx) * kEntryWords + (lane & 15));
+    desc = load_word_untracked(ents + int64_t(idx) * kEntryWords + (lane & 15));
   };
   // word i of the entry (second = false) or of the one after it
   auto desc_word = [&](int32_t dw, bool second, int i) __attribute__((always_inline)) -> int {
@@ -556,7 +597,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     int64_t off = 0;
     if (exists) {
       const int r = desc_word(dw, second, cw::kEntR), nv = desc_word(dw, second, cw::kEntNvalid);
-      const int64_t row = int64_t(desc_word(dw, second, cw::kEntCu0)) + desc_word(dw, second, cw::kEntRow0) + pos;
+      const int64_t row = int64_t(desc_word(dw, second, cw::kEntQrow)) + pos;
       const int hd = desc_word(dw, second, cw::kEntG) * a.group + hh;
       off = (r >= 0 && hh < a.group && pos < nv) ? (row * a.hq + hd) * D : 0;
     }
@@ -587,29 +628,36 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 
+  // Output rows of the staged read-back (unsplit kernel): the lanes reading
+  // staged row rr hold column m' = 32 wave + rr of the tile, i.e. head m' / T
+  // and position m' % T (T = a.per_tile; the quotient by a multiply, exact for
+  // m' < 256).
+  const uint32_t tdiv = (65536u + uint32_t(a.per_tile) - 1) / uint32_t(a.per_tile);
+
   for (int e = blockIdx.x; e < a.num_entries; e += grid) {
     // the words landed before the previous entry's last step barrier (or the
     // first steps' wait)
     asm volatile("" : "+v"(desc));
     const int32_t dw = desc;
-    int32_t f[cw::kEntFields];
-#pragma unroll
-    for (int i = 0; i < cw::kEntFields; ++i) f[i] = desc_word(dw, false, i);
     // the end of the queue, or an entry that is not the one the planner wrote
-    if (f[cw::kEntR] < 0 || uint32_t(desc_word(dw, false, cw::kEntCheck)) != cw::entry_check(a.fp_lo, a.fp_hi, f))
+    if (desc_word(dw, false, cw::kEntR) < 0 ||
+        uint32_t(desc_word(dw, false, cw::kEntCheck)) != cw::entry_tag(a.fp_lo, a.fp_hi, uint32_t(e)))
       break;
     // where the next entry's Q comes from (the split kernel has no registers
     // to spare for a prefetch)
     const u32x4* q_next = SPLIT ? nullptr : q_source(dw, true, e + grid < a.num_entries);
-    const int g = f[cw::kEntG], row0 = f[cw::kEntRow0], nvalid = f[cw::kEntNvalid];
-    const int cu0 = f[cw::kEntCu0], P = f[cw::kEntP];
-    const int kbeg = f[cw::kEntKbeg], kend = f[cw::kEntKend];
-    const int split = SPLIT ? f[cw::kEntSplit] : 0;
-    const int nsteps = kend - kbeg;
+    const int g = desc_word(dw, false, cw::kEntG), row0 = desc_word(dw, false, cw::kEntRow0);
+    const int nvalid = desc_word(dw, false, cw::kEntNvalid), P = desc_word(dw, false, cw::kEntP);
+    const int qrow0 = desc_word(dw, false, cw::kEntQrow);
+    const int kbeg = desc_word(dw, false, cw::kEntKbeg);
+    const int nsteps = desc_word(dw, false, cw::kEntKend) - kbeg;
+    // steps [0, n_full) are visible to every row of the entry (no mask)
+    const int n_full = desc_word(dw, false, cw::kEntNfull);
+    const int split = SPLIT ? desc_word(dw, false, cw::kEntSplit) : 0;
 
     const bool row_ok = (hh < a.group) && (pos < nvalid);
     const int qpos = P + row0 + pos;  // keys 0 .. qpos are visible
-    const int64_t qrow = int64_t(cu0) + row0 + pos;
+    const int64_t qrow = int64_t(qrow0) + pos;
     const int head = g * a.group + hh;
 
     if (SPLIT && nsteps == 0) {   // no key of this run: an empty part
@@ -702,23 +750,20 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       }
     };
     // Probabilities of element pair i (of 16) of S: 2^(s - m) for two keys,
-    // packed to bf16, and their sum added to ls.
-    auto prob_pair = [&](const f32x16 (&sc)[2], int i, float& ls) __attribute__((always_inline)) -> uint32_t {
+    // packed to bf16.
+    auto prob_pair = [&](const f32x16 (&sc)[2], int i) __attribute__((always_inline)) -> uint32_t {
       const int kk = i >> 2, jj = i & 3, h = kk >> 1, e = (kk & 1) * 8 + 2 * jj;
-      const uint32_t w = pack_bf16x2(__builtin_amdgcn_exp2f(sc[h][e]), __builtin_amdgcn_exp2f(sc[h][e + 1]));
+      return pack_bf16x2(__builtin_amdgcn_exp2f(sc[h][e]), __builtin_amdgcn_exp2f(sc[h][e + 1]));
+    };
+    // ls += the two probabilities of a packed pair (the row sum uses the
+    // rounded probabilities the PV product uses)
+    auto sum_pair = [&](uint32_t w, float& ls) __attribute__((always_inline)) {
       ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, ls, false);
-      return w;
     };
     auto pack_pb = [&](const uint32_t (&w)[16], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk], w[4 * kk + 1], w[4 * kk + 2], w[4 * kk + 3]});
     };
-    // Phase A of a step: S(j+1) = K Q^T from the stage at kb (accumulators from
-    // -m) interleaved with the probabilities of S(j) (sc -> pb). Each group is
-    // one MFMA, the operand read three MFMAs ahead and one element pair of the
-    // softmax; an empty use at the group's end pins the pair's arithmetic
-    // between this MFMA and the next (the compiler would otherwise gather it
-    // after the last MFMA).
     // Where a step's copies go: the first half after MFMAs 0, E, 2E, .. of
     // phase A, the second half likewise in phase B; a step without phase A
     // (an entry's last) puts all of them in phase B.
@@ -735,11 +780,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         copy_part(HALF_C + i / E);
       }
     };
+    // Phase A of a step: S(j+1) = K Q^T from the stage at kb (accumulators
+    // from -m) interleaved with the probabilities of S(j) (sc -> pb). Each
+    // group is one MFMA, the operand read three MFMAs ahead and one element
+    // pair of the softmax, fenced by a scheduling barrier so that the groups
+    // keep this order (the compiler would otherwise gather the vector work
+    // after the last MFMA and reorder the MFMAs, collapsing the read-ahead);
+    // an empty use pins each pair in its group.
     auto phase_a = [&](int kb, const f32x16 (&sc)[2], f32x16 (&sn)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
       constexpr int N = 2 * KS;
       constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
       uint32_t w[16];
-      float ls[2] = {0.f, 0.f};
       bf16x8 kf[3];
 #pragma unroll
       for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, i);
@@ -751,12 +802,12 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         copies_a(i);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
-          w[i * PER + u] = prob_pair(sc, i * PER + u, ls[(i * PER + u) & 1]);
+          w[i * PER + u] = prob_pair(sc, i * PER + u);
           asm volatile("" :: "v"(w[i * PER + u]));
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
       pack_pb(w, pb);
-      l_run += ls[0] + ls[1];
     };
     // The last step of an entry (no next scores): O^T += V^T P^T with the
     // probabilities of 16-key slice kk + 1 formed while the PV MFMAs of slice
@@ -770,7 +821,10 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, i);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = prob_pair(sc, i, ls[i & 1]);
+      for (int i = 0; i < 4; ++i) {
+        w[i] = prob_pair(sc, i);
+        sum_pair(w[i], ls[i & 1]);
+      }
       bf16x8 pk = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -783,7 +837,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
           for (int u = 0; u < PER; ++u) {
             const int q = (kk + 1) * 4 + (i % DT) * PER + u;
-            w[q] = prob_pair(sc, q, ls[q & 1]);
+            w[q] = prob_pair(sc, q);
+            sum_pair(w[q], ls[q & 1]);
             asm volatile("" :: "v"(w[q]));
           }
         } else {
@@ -791,16 +846,20 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         }
         if (i % DT == DT - 1 && kk + 1 < 4)
           pk = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk + 4], w[4 * kk + 5], w[4 * kk + 6], w[4 * kk + 7]});
+        __builtin_amdgcn_sched_barrier(0);
       }
       l_run += ls[0] + ls[1];
     };
     // Phase B of a step: O^T += V^T P^T from the stage at vb (operand reads
-    // three ahead), interleaved with the row maximum of the next scores sn
-    // (already masked); returns it relative to the base.
+    // three ahead), in groups like phase A's, with the row sums of P (first)
+    // and the row maximum of the next scores sn (already masked; last, so that
+    // the last MFMAs of phase A have completed); returns the maximum relative
+    // to the base.
     auto phase_b = [&](int vb, const bf16x8 (&pb)[4], const f32x16 (&sn)[2]) __attribute__((always_inline)) -> float {
       constexpr int N = 4 * DT;
-      constexpr int PER = 16 / N;   // max3 operations per MFMA
+      constexpr int PER = 16 / N;   // sums and max3 operations per MFMA
       float x[2] = {-INFINITY, -INFINITY};
+      float ls[2] = {0.f, 0.f};
       bf16x8 vf[3];
 #pragma unroll
       for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, i);
@@ -812,11 +871,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         copies_b(i, false);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
-          const int q = i * PER + u, h = q & 1, e = (q >> 1) * 2;
+          const int q = i * PER + u;
+          sum_pair(__builtin_bit_cast(u32x4, pb[q >> 2])[q & 3], ls[q & 1]);
+          asm volatile("" :: "v"(ls[q & 1]));
+          // the max starts two groups late; the first pairs go with the end
+          const int qm = (q + 2) % 16, h = qm & 1, e = (qm >> 1) * 2;
           x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
           asm volatile("" :: "v"(x[h]));
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
+      l_run += ls[0] + ls[1];
       return max_pair32(fmaxf(x[0], x[1]));
     };
     // Moves the base up by the step maximum when it exceeds the base by kLazy.
@@ -835,8 +900,6 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     };
     auto kbase = [&](int pp) { return (pp & (kStages - 1)) * KTILE; };
     auto vbase = [&](int pp) { return v_off + (pp & (kStages - 1)) * VTILE; };
-    // steps [0, n_full) are visible to every row of the entry (no mask)
-    const int n_full = max(0, min(nsteps, (P + row0 + 1) / kKv - kbeg));
 
     // ---- S(0) with the exact row maximum as base
     f32x16 sa[2], sb[2];
@@ -855,8 +918,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       for (int e2 = 0; e2 < 16; ++e2) mneg[e2] = -m0;
     }
 
+    const int last = nsteps - 1;
+    // Two steps before its last one, an entry brings the next entry's queries
+    // into L2 (one 128-byte line per lane), so that their load at the last
+    // step does not wait for HBM. (Entries of one or two steps skip it.)
+    const int touch_at = SPLIT ? -1 : last - 2;
+    auto touch_q = [&]() __attribute__((always_inline)) {
+      touch_line(reinterpret_cast<const uint8_t*>(q_next) + half * 128, own_area);
+    };
     // Step j < nsteps - 1 at ring position p: current S in sc, next S into sn.
     auto step = [&](int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
+      if (j == touch_at) touch_q();
       const bool direct = issue(p + kAhead, true);
       rebase(sc);
       bf16x8 pb[4];
@@ -866,7 +938,6 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       step_barrier(direct);
       ++p;
     };
-    const int last = nsteps - 1;
     int j = 0;
     // two steps per iteration so the S buffers alternate without copies
     for (; j + 1 < last; j += 2) {
@@ -916,13 +987,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       constexpr int SROWS = G::STAGING / RB;   // rows staged per round
       constexpr int RPI = 64 / NC;             // rows per read-back instruction
       const float inv = row_ok ? 1.f / l_tot : 0.f;
-      // this lane's output row (suffix row x Hq + head), -1 for none
-      const int orow = row_ok ? int(qrow * a.hq + head) : -1;
       uint8_t* stg = lds + G::RING + wave * G::STAGING;
+      // Opaque copies of the values the addresses below derive from: without
+      // them the compiler computes those (entry- or lane-invariant) addresses
+      // before the steps and keeps them live across the step loop.
+      int ln = lane, q0 = qrow0, nv = nvalid, hg = g * a.group;
+      asm volatile("" : "+v"(ln), "+s"(q0), "+s"(nv), "+s"(hg));
+      const int l32e = ln & 31, halfe = ln >> 5;
 #pragma unroll
       for (int rd = 0; rd < 32 / SROWS; ++rd) {
-        if (l32 / SROWS == rd) {
-          const int r = l32 % SROWS;
+        if (l32e / SROWS == rd) {
+          const int r = l32e % SROWS;
 #pragma unroll
           for (int t = 0; t < DT; ++t)
 #pragma unroll
@@ -930,15 +1005,19 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
               const int c = t * 4 + gq;   // 16-byte chunk: d = 8 c .. 8 c + 7
               const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
                             pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
-              *reinterpret_cast<u32x2*>(stg + r * RB + ((c ^ G::kswz(r)) << 4) + half * 8) = w;
+              *reinterpret_cast<u32x2*>(stg + r * RB + ((c ^ G::kswz(r)) << 4) + halfe * 8) = w;
             }
         }
 #pragma unroll
         for (int q = 0; q < SROWS / RPI; ++q) {
-          const int r = q * RPI + lane / NC, c = lane % NC;
+          const int r = q * RPI + ln / NC, c = ln % NC;
           const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * RB + ((c ^ G::kswz(r)) << 4));
-          const int ro = __shfl(orow, rd * SROWS + r);
-          if (ro >= 0) *reinterpret_cast<u32x4*>(a.out + int64_t(ro) * D + c * 8) = v;
+          // the staged row's column of the tile, its head and position
+          const uint32_t mr = uint32_t(wave * 32 + rd * SROWS + r);
+          const int hr = int((mr * tdiv) >> 16);
+          const int pr = int(mr) - hr * a.per_tile;
+          if (hr < a.group && pr < nv)
+            *reinterpret_cast<u32x4*>(a.out + ((int64_t(q0) + pr) * a.hq + hg + hr) * D + c * 8) = v;
         }
       }
     }
