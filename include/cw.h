@@ -307,7 +307,8 @@ cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* p
  * CW_EINVAL: NULL pointer, batch < 1, Hq % Hkv != 0, P_r % bs != 0, cu not
  * non-decreasing from 0, ceil(L_r / bs) > bt_stride, softmax_scale not finite
  * and positive, a plan built for another batch description or with splits.
- * CW_EUNSUPPORTED: head_dim not 64/128, block_size != 16, Hq / Hkv > 128.
+ * CW_EUNSUPPORTED: head_dim not 64/128, block_size != 16, Hq / Hkv > 128,
+ *   more than 65536 KV heads.
  * CW_EHIP: launch failure. */
 cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void* v_cache,
                                  const int32_t* block_table, int32_t bt_stride,

@@ -13,6 +13,14 @@ destination registers before a covering wait.
 A load counts as untracked when it sits in an inline-asm block without a wait
 of its own; `s_waitcnt vmcnt(k)` covers a load on a path where at least k
 memory instructions were issued after it.
+
+Paths follow branch conditions in one form the compiler uses for wave-uniform
+if/else: an if/else becomes two sequential `if`s on one SGPR-pair flag F set
+to all lanes (-1) or none (0) by s_mov_b64, each testing `vcc = exec & F` (or
+`exec & ~F`) with s_cbranch_vccz/vccnz. A path knows F from its last constant
+assignment until an instruction writes F, and takes only the branch direction
+that value gives (exec is taken to be nonzero). Flags of any other origin (a
+per-lane compare, say) are not evaluated: both directions are followed.
 """
 from __future__ import annotations
 
@@ -68,6 +76,56 @@ def parse(lines: list[str]):
     return insts, labels, untracked
 
 
+_SPAIR = re.compile(r'^s\[(\d+):(\d+)\]$')
+_SREG1 = re.compile(r'^s(\d+)$')
+# mnemonics whose first operand is not a register they write
+_NO_DEST = ('s_cmp', 's_bitcmp', 's_cbranch', 's_branch', 's_waitcnt', 's_barrier', 's_nop', 's_endpgm',
+            's_setprio', 's_sleep', 's_sendmsg', 'global_store', 'buffer_store', 'ds_write', 'scratch_store')
+
+
+def _operands(text: str) -> list[str]:
+    parts = text.split(None, 1)
+    return [x.strip() for x in parts[1].split(',')] if len(parts) > 1 else []
+
+
+def _sdest(text: str) -> set[int] | None:
+    """SGPR numbers an instruction writes through its first operand; None when
+    it writes vcc (as a first operand or implicitly, v_cmp*_e32)."""
+    op = text.split()[0]
+    if op.startswith('v_cmp') and op.endswith('_e32'):
+        return None
+    if op.startswith(_NO_DEST):
+        return set()
+    ops = _operands(text)
+    if not ops:
+        return set()
+    first = ops[0]
+    if first == 'vcc':
+        return None
+    m = _SPAIR.match(first)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = _SREG1.match(first)
+    if m:
+        return {int(m.group(1))}
+    return set()
+
+
+def _vcc_flag(text: str):
+    """(F, negated) when the instruction is `s_and_b64 vcc, exec, F` or
+    `s_andn2_b64 vcc, exec, F` with F an SGPR pair, else None."""
+    op = text.split()[0]
+    if op not in ('s_and_b64', 's_andn2_b64'):
+        return None
+    ops = _operands(text)
+    if len(ops) != 3 or ops[0] != 'vcc' or ops[1] != 'exec':
+        return None
+    m = _SPAIR.match(ops[2])
+    if not m:
+        return None
+    return (int(m.group(1)), int(m.group(2))), op == 's_andn2_b64'
+
+
 def _successors(insts, labels, i):
     op = insts[i].split()[0]
     if op == 's_endpgm':
@@ -79,19 +137,83 @@ def _successors(insts, labels, i):
     return [i + 1]
 
 
+def _step(insts, labels, i, vflag, known):
+    """Successor states (instruction, vflag, known) of instruction i: the flag
+    tests of s_cbranch_vccz/vccnz, and forgetting flags an instruction writes."""
+    text = insts[i]
+    op = text.split()[0]
+    if op in ('s_cbranch_vccz', 's_cbranch_vccnz') and vflag is not None:
+        flag, neg = vflag
+        taken_f = (not neg) if op == 's_cbranch_vccnz' else neg   # F under which the branch is taken
+        kv = dict(known)
+        out = []
+        for succ, fval in ((labels[text.split()[1]], taken_f), (i + 1, not taken_f)):
+            if flag in kv and kv[flag] != fval:
+                continue
+            out.append((succ, vflag, known))
+        return out
+    f = _vcc_flag(text)
+    if f is not None:
+        vflag = f
+    else:
+        w = _sdest(text)
+        if w is None:
+            vflag = None
+        elif w:
+            known = frozenset(x for x in known if not (set(range(x[0][0], x[0][1] + 1)) & w))
+            if vflag is not None and set(range(vflag[0][0], vflag[0][1] + 1)) & w:
+                vflag = None
+            # a flag set to a constant: all lanes (-1) or none (0)
+            ops = _operands(text)
+            m = _SPAIR.match(ops[0]) if op == 's_mov_b64' and len(ops) == 2 else None
+            if m and ops[1] in ('-1', '0'):
+                known = known | {((int(m.group(1)), int(m.group(2))), ops[1] == '-1')}
+    return [(s, vflag, known) for s in _successors(insts, labels, i)]
+
+
+def _entry_facts(insts, labels):
+    """For each instruction, the (vflag, known flags) that hold on every path
+    from the function's entry to it (None: unreachable)."""
+    state: list = [None] * len(insts)
+    if not insts:
+        return state
+    state[0] = (None, frozenset())
+    work = [0]
+    while work:
+        i = work.pop()
+        if i >= len(insts) or state[i] is None:
+            continue
+        vflag, known = state[i]
+        for succ, v2, k2 in _step(insts, labels, i, vflag, known):
+            if succ >= len(insts):
+                continue
+            old = state[succ]
+            new = (v2, k2) if old is None else (old[0] if old[0] == v2 else None, old[1] & k2)
+            if new != old:
+                state[succ] = new
+                work.append(succ)
+    return state
+
+
 def hazards(lines: list[str]) -> list[tuple[str, str]]:
-    """(load, offending instruction) pairs over every path of one function."""
+    """(load, offending instruction) pairs over every feasible path of one
+    function (feasible as far as the flag tests described above tell)."""
     insts, labels, loads = parse(lines)
+    facts = _entry_facts(insts, labels)
     found = []
     for li in loads:
         dst = vregs(insts[li].split()[1].rstrip(','))
+        if facts[li] is None:
+            continue
         seen = set()
-        stack = [(li + 1, 0)]
+        # (instruction, memory instructions issued since the load, the flag the
+        # last vcc write tests, known flag values)
+        stack = [(s, 0, v, k) for s, v, k in _step(insts, labels, li, *facts[li])]
         while stack:
-            i, younger = stack.pop()
+            i, younger, vflag, known = stack.pop()
             if i >= len(insts):
                 continue
-            key = (i, min(younger, 64))
+            key = (i, min(younger, 64), vflag, known)
             if key in seen:
                 continue
             seen.add(key)
@@ -107,8 +229,8 @@ def hazards(lines: list[str]) -> list[tuple[str, str]]:
                 found.append((insts[li], text))
                 continue
             nxt = younger + (1 if _VMEM.match(text) else 0)
-            for s in _successors(insts, labels, i):
-                stack.append((s, nxt))
+            for s, v2, k2 in _step(insts, labels, i, vflag, known):
+                stack.append((s, nxt, v2, k2))
     return found
 
 

@@ -24,6 +24,7 @@ constexpr int kTileRows = 256;   // packed query rows (heads x positions) per wo
 constexpr int kKvTile = 64;      // keys staged in LDS per step
 constexpr int kNumXcd = 8;       // L2 partitions; workgroup i runs on partition i % 8
 constexpr int kMaxGroup = 128;   // query heads per KV head supported
+constexpr int kMaxKvHeads = 65536;   // KV heads supported by the attention calls
 
 constexpr int kNumCu = 256;      // compute units: the attention grid's persistent workgroups
 constexpr int kMaxSplits = 64;   // key runs per tile on the split path

@@ -206,9 +206,9 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 // LDS layouts. A load-to-LDS instruction writes 64 x 16 bytes contiguously in
 // lane order, so swizzles are applied on the global side (each lane fetches
 // the 16 bytes that belong at its LDS slot).
-//  * K stages: row-major [key][d] (RB bytes per row); 16-byte chunk c of row r
-//    is stored at c ^ kswz(r), which puts the 16 rows of every operand read
-//    phase on distinct banks.
+//  * K stages: each block of 16 keys chunk-major, [16-byte chunk c][key r]
+//    at c 256 + r 16: the 16 keys a read phase takes sit on distinct banks,
+//    and a lane's operand reads differ only by immediate offsets.
 //  * V stages (after the four K stages): each block as in the cache,
 //    [block][d][16 keys], 32-byte rows with the two 16-byte halves of row d
 //    swapped when bit 3 of d is set (conflict-free operand reads).
@@ -297,7 +297,6 @@ constexpr int kAhead = 3;    // the cursor copies a step this many steps before 
 template <int D>
 struct AttnGeom {
   static constexpr int RB = 2 * D;              // bytes per K row
-  static constexpr int NC = D / 8;              // 16-byte chunks per K row
   static constexpr int KTILE = kKv * RB;        // K of one step
   static constexpr int BLK = D * 2 * kBs;       // one V^T block (D rows of 16 keys)
   static constexpr int VTILE = (kKv / kBs) * BLK;
@@ -305,14 +304,11 @@ struct AttnGeom {
   static constexpr int RING = KREG + kStages * VTILE;
   static constexpr int STAGING = 4096;          // per-wave area after the ring
   static constexpr int LDS = RING + kAttnWaves * STAGING;
-  static constexpr int RPL = 1024 / RB;         // K rows per 1 KB copy
   static constexpr int LPW = kBs * RB / 1024;   // 1 KB copies per block and tensor
   static constexpr int KS = D / 16;             // MFMA k-steps over D
   static constexpr int DT = D / 32;             // 32-row output tiles over D
-  // chunk swizzle of K row r (rows of 256 bytes: 16 chunks; of 128 bytes: 8)
-  __device__ static int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
   static_assert(LDS <= 160 * 1024, "LDS budget");
-  static_assert((kStages - 1) * KTILE + 32 * RB < 65536, "K read offsets are immediates");
+  static_assert(32 * RB + (KS - 1) * 512 < 65536, "K read offsets are immediates");
   static_assert((kStages - 1) * VTILE + 3 * BLK + (DT - 1) * 1024 < 65536, "V read offsets are immediates");
 };
 
@@ -369,7 +365,7 @@ template <int D, bool SPLIT>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void suffix_prefill_attn_kernel(const AttnArgs a) {
   using G = AttnGeom<D>;
-  constexpr int KS = G::KS, DT = G::DT, RB = G::RB, NC = G::NC, LPW = G::LPW, RPL = G::RPL;
+  constexpr int KS = G::KS, DT = G::DT, RB = G::RB, LPW = G::LPW;
   constexpr int KTILE = G::KTILE, BLK = G::BLK, VTILE = G::VTILE, KREG = G::KREG;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[G::LDS];
   const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
@@ -391,8 +387,10 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   const int bs = wave >> 1;
   const bool is_v = (wave & 1) != 0;
   const uint8_t* const cache = reinterpret_cast<const uint8_t*>(is_v ? a.vc : a.kc);
-  // bytes from one physical block of a tensor to the next
-  const int64_t blk_bytes = int64_t(a.hkv) * (kBs * RB);
+  // bytes from one physical block of a tensor to the next (below 2^28: the
+  // host refuses more than kMaxKvHeads KV heads), multiplied by a block ID as
+  // two 32-bit values
+  const uint32_t blk_bytes = uint32_t(a.hkv) * (kBs * RB);
   // Per-lane source offset inside a block and LDS destination of copy i
   // (relative to the wave's block slot in a stage; lane l lands at +16 l).
   uint32_t src_off[LPW];
@@ -402,8 +400,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       const int d = 32 * i + (lane >> 1);
       src_off[i] = d * 32 + (((lane & 1) ^ ((lane >> 4) & 1)) << 4);
     } else {
-      const int row = RPL * i + lane / NC;   // row inside the block
-      src_off[i] = row * RB + (((lane % NC) ^ G::kswz(row)) << 4);
+      // K blocks are staged chunk-major: 16-byte chunk c of row r at c 256 + r 16
+      src_off[i] = (lane & 15) * RB + ((4 * i + (lane >> 4)) << 4);
     }
   }
   // LDS address of this wave's block slot in ring position 0
@@ -424,7 +422,9 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   int c_whole = 0;       // logical blocks below this hold 16 keys of the prompt
   int c_last = 0;        // last logical block inside the prompt
   int c_L = 0;           // prompt length of the cursor's request
+  int c_fast = 0;        // steps from the cursor's step that take the fast path of issue()
   const int32_t* c_row = a.bt;   // block-table row of the cursor's request
+  const int32_t* c_ptr = a.bt;   // table word of this wave's block at the cursor's step
   const uint8_t* c_src = cache;  // this wave's tensor at the cursor's KV head
   bool cdone = false;
   auto entry_word_addr = [&](int e) __attribute__((always_inline)) -> const int32_t* {
@@ -447,7 +447,13 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     c_whole = c_L / kBs;
     c_last = (c_L + kBs - 1) / kBs - 1;
     c_row = a.bt + int64_t(r) * a.bt_stride;
+    c_ptr = c_row + c_lb;
     c_src = cache + int64_t(__builtin_amdgcn_readlane(cdesc, cw::kEntG)) * (kBs * RB);
+    // Fast steps: not the entry's last (whose issue() enters the next entry),
+    // the block whole (lb < c_whole) and the next step's table word inside
+    // the prompt's blocks (lb + 4 <= c_last), so that it needs no clamp.
+    const int lim = min(c_whole, c_last - (kKv / kBs - 1));
+    c_fast = min(c_left - 1, max(0, (lim - c_lb + kKv / kBs - 1) / (kKv / kBs)));
     ce += grid;
     cdesc = load_word_untracked(entry_word_addr(ce));
   };
@@ -470,7 +476,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // harmless word (the plan's first) is loaded.
   int32_t bword = 0;
   auto cursor_load = [&]() __attribute__((always_inline)) {
-    bword = load_word_untracked_s(cdone ? a.plan : c_row + min(c_lb, c_last));
+    c_ptr = c_row + min(c_lb, c_last);
+    bword = load_word_untracked_s(cdone ? a.plan : c_ptr);
   };
   cursor_enter();
   cursor_load();
@@ -490,19 +497,40 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // through registers and waited for at once). The table word it reads was
   // completed by the wait before this call.
   auto issue = [&](int p, bool spread) __attribute__((always_inline)) -> bool {
+    asm volatile("" : "+v"(bword));
+    const int raw = __builtin_amdgcn_readfirstlane(bword);
+    const uint32_t dst = slot0 + uint32_t(p & (kStages - 1)) * stage_stride;
+    // fast path: a whole block inside the pool, the next word inside the
+    // prompt's blocks, the cursor stays in its entry (c_fast > 0 implies
+    // !cdone)
+    if (c_fast > 0 && uint32_t(raw) < uint32_t(a.num_blocks)) {
+      const uint8_t* src = c_src + uint64_t(uint32_t(raw)) * blk_bytes;
+      --c_fast;
+      --c_left;
+      c_lb += kKv / kBs;
+      c_ptr += kKv / kBs;
+      bword = load_word_untracked_s(c_ptr);
+      if (spread) {
+        cp_src = reinterpret_cast<uintptr_t>(src);
+        cp_dst = dst;
+        cp_stride = 1024;
+      } else {
+#pragma unroll
+        for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
+      }
+      return true;
+    }
     cp_src = reinterpret_cast<uintptr_t>(cache);
     cp_dst = own_area;
     cp_stride = 0;
     if (cdone) return false;
-    asm volatile("" : "+v"(bword));
-    const int raw = __builtin_amdgcn_readfirstlane(bword);
     const int lb = c_lb, L = c_L;
     // physical block, or -1 past the prompt / outside the pool
     const int b = (lb <= c_last && uint32_t(raw) < uint32_t(a.num_blocks)) ? raw : -1;
     const bool whole = b >= 0 && lb < c_whole;
-    const uint8_t* src = c_src + int64_t(b < 0 ? 0 : b) * blk_bytes;
-    const uint32_t dst = slot0 + uint32_t(p & (kStages - 1)) * stage_stride;
+    const uint8_t* src = c_src + uint64_t(uint32_t(b < 0 ? 0 : b)) * blk_bytes;
     c_lb += kKv / kBs;
+    c_fast = max(0, c_fast - 1);
     if (--c_left == 0) cursor_enter();
     cursor_load();
     if (whole) {   // wave-uniform: the whole block is valid
@@ -530,7 +558,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
       } else {
-        const bool ok = b >= 0 && key0 + RPL * i + lane / NC < L;
+        const bool ok = b >= 0 && key0 + (lane & 15) < L;
         v = ok ? v : zero;
       }
       *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
@@ -551,18 +579,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   };
 
   // ---- per-lane LDS read offsets (ring position 0; a position adds its stride)
-  // K operand: row 32 h + pi(l32), logical chunk 2 s + half.
+  // K operand: key 32 h + pi(l32) (block 2 h + l32 / 16, row pi(l32) % 16),
+  // chunk 2 s + half; in the chunk-major block layout that is the lane's base
+  // plus h 32 RB + s 512.
   const int k_row = (l32 & ~12) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
-  int k_off[KS];
-#pragma unroll
-  for (int s = 0; s < KS; ++s) k_off[s] = k_row * RB + (((2 * s + half) ^ G::kswz(k_row)) << 4);
+  int k_off = (l32 >> 4) * (kBs * RB) + half * 256 + (k_row & 15) * 16;
   // V operand: block kk, row d = 32 t + l32, logical half = half.
   int v_off = KREG + l32 * 32 + ((half ^ ((l32 >> 3) & 1)) << 4);
   // Hide the bases' known bits from the compiler: otherwise it rewrites
   // base + constant as base | constant, which it cannot fold into the LDS
   // instructions' offset field, and keeps one register per read instead.
-#pragma unroll
-  for (int s = 0; s < KS; ++s) asm volatile("" : "+v"(k_off[s]));
+  asm volatile("" : "+v"(k_off));
   asm volatile("" : "+v"(v_off));
   auto rd16 = [&](int addr) __attribute__((always_inline)) -> bf16x8 {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lds + addr));
@@ -732,7 +759,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // stage at kb; V operand of PV MFMA i (16-key slice i / DT, output tile
     // i % DT) of the stage at vb.
     auto rdk = [&](int kb, int i) __attribute__((always_inline)) -> bf16x8 {
-      return rd16(kb + k_off[i >> 1] + (i & 1) * 32 * RB);
+      return rd16(kb + (i & 1) * 32 * RB + (i >> 1) * 512);
     };
     auto rdv = [&](int vb, int i) __attribute__((always_inline)) -> bf16x8 {
       return rd16(vb + (i / DT) * BLK + (i % DT) * 1024);
@@ -898,7 +925,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         for (int t = 0; t < DT; ++t) oacc[t] *= alpha;
       }
     };
-    auto kbase = [&](int pp) { return (pp & (kStages - 1)) * KTILE; };
+    auto kbase = [&](int pp) { return k_off + (pp & (kStages - 1)) * KTILE; };
     auto vbase = [&](int pp) { return v_off + (pp & (kStages - 1)) * VTILE; };
 
     // ---- S(0) with the exact row maximum as base
@@ -981,12 +1008,21 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     } else {
       // The output goes through this wave's staging area: a lane holds 4
       // consecutive d of its row per (t, gq), so direct stores would write 32
-      // rows in 8-byte pieces per instruction. Rows are staged (16-byte chunks
-      // swizzled like K rows) and read back NC lanes per row, so that each
-      // store covers whole rows.
-      constexpr int SROWS = G::STAGING / RB;   // rows staged per round
-      constexpr int RPI = 64 / NC;             // rows per read-back instruction
-      const float inv = row_ok ? 1.f / l_tot : 0.f;
+      // rows in 8-byte pieces per instruction. Each round stages a range of d
+      // (HD values) of all 32 rows and reads it back as rows of 16-byte
+      // chunks, so that each store covers whole 128-byte lines of HD values
+      // (16-byte chunk c of staged row r at position c ^ (r % CPR):
+      // conflict-free writes and reads). Lanes read what other lanes wrote:
+      // the hardware keeps a wave's LDS accesses in order, and empty asm
+      // statements with a memory clobber keep the compiler from reusing, for
+      // a lane, values it loaded before another lane's writes (as it may, for
+      // memory it sees no other thread write).
+      constexpr int HD = G::STAGING / (32 * 2);   // d values per round (64)
+      constexpr int CPR = HD / 8;                // 16-byte chunks per staged row
+      constexpr int TPR = HD / 32;               // output tiles per round
+      constexpr int RPI = 64 / CPR;              // staged rows per read instruction
+      static_assert(D % HD == 0 && CPR == 8, "staging rounds");
+      const float inv = row_ok ? __builtin_amdgcn_rcpf(l_tot) : 0.f;
       uint8_t* stg = lds + G::RING + wave * G::STAGING;
       // Opaque copies of the values the addresses below derive from: without
       // them the compiler computes those (entry- or lane-invariant) addresses
@@ -995,29 +1031,34 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       asm volatile("" : "+v"(ln), "+s"(q0), "+s"(nv), "+s"(hg));
       const int l32e = ln & 31, halfe = ln >> 5;
 #pragma unroll
-      for (int rd = 0; rd < 32 / SROWS; ++rd) {
-        if (l32e / SROWS == rd) {
-          const int r = l32e % SROWS;
+      for (int rd = 0; rd < D / HD; ++rd) {
 #pragma unroll
-          for (int t = 0; t < DT; ++t)
+        for (int tt = 0; tt < TPR; ++tt)
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-              const int c = t * 4 + gq;   // 16-byte chunk: d = 8 c .. 8 c + 7
-              const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
-                            pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
-              *reinterpret_cast<u32x2*>(stg + r * RB + ((c ^ G::kswz(r)) << 4) + halfe * 8) = w;
-            }
+          for (int gq = 0; gq < 4; ++gq) {
+            const int t = rd * TPR + tt, c = tt * 4 + gq;   // d = 32 t + 8 gq + 4 half ..
+            const u32x2 w{pack_bf16x2(oacc[t][gq * 4 + 0] * inv, oacc[t][gq * 4 + 1] * inv),
+                          pack_bf16x2(oacc[t][gq * 4 + 2] * inv, oacc[t][gq * 4 + 3] * inv)};
+            *reinterpret_cast<u32x2*>(stg + l32e * (HD * 2) + ((c ^ (l32e % CPR)) << 4) + halfe * 8) = w;
+          }
+        asm volatile("" ::: "memory");
+        // all of the round's reads first, then the stores of the rows that exist
+        u32x4 v[32 / RPI];
+#pragma unroll
+        for (int q = 0; q < 32 / RPI; ++q) {
+          const int r = q * RPI + ln / CPR, c = ln % CPR;
+          v[q] = *reinterpret_cast<const u32x4*>(stg + r * (HD * 2) + ((c ^ (r % CPR)) << 4));
         }
+        asm volatile("" ::: "memory");
 #pragma unroll
-        for (int q = 0; q < SROWS / RPI; ++q) {
-          const int r = q * RPI + ln / NC, c = ln % NC;
-          const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r * RB + ((c ^ G::kswz(r)) << 4));
+        for (int q = 0; q < 32 / RPI; ++q) {
+          const int r = q * RPI + ln / CPR, c = ln % CPR;
           // the staged row's column of the tile, its head and position
-          const uint32_t mr = uint32_t(wave * 32 + rd * SROWS + r);
+          const uint32_t mr = uint32_t(wave * 32 + r);
           const int hr = int((mr * tdiv) >> 16);
           const int pr = int(mr) - hr * a.per_tile;
           if (hr < a.group && pr < nv)
-            *reinterpret_cast<u32x4*>(a.out + ((int64_t(q0) + pr) * a.hq + hg + hr) * D + c * 8) = v;
+            *reinterpret_cast<u32x4*>(a.out + ((int64_t(q0) + pr) * a.hq + hg + hr) * D + rd * HD + c * 8) = v[q];
         }
       }
     }
@@ -1129,6 +1170,7 @@ cw_status check_attn(const char* what, const void* q, const void* k_cache, const
   if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, w + ": block_size must be 16");
   const int group = num_q_heads / num_kv_heads;
   if (group > cw::kMaxGroup) return cw::fail(CW_EUNSUPPORTED, w + ": more than 128 query heads per KV head");
+  if (num_kv_heads > cw::kMaxKvHeads) return cw::fail(CW_EUNSUPPORTED, w + ": more than 65536 KV heads");
   cw_status st = cw::check_batch(cu_suffix_host, prefix_len_host, batch, block_size, bt_stride, &L->rows);
   if (st != CW_OK) return st;
   AttnArgs& a = L->args;

@@ -54,3 +54,27 @@ def test_check_raises_with_the_function_name():
         asm_check.check(text)
     with pytest.raises(RuntimeError, match="no function"):
         asm_check.check(_fn("\ts_nop 0\n"))
+
+
+def test_flag_tests_on_a_lane_mask_follow_both_directions():
+    # if (F) { load } ; if (!F) { use } with F a per-lane compare: some lanes may
+    # take each arm, so the use after the load is reported
+    body = ("\tv_cmp_gt_i32_e64 s[12:13], 3, v1\n\ts_and_b64 vcc, exec, s[12:13]\n\ts_cbranch_vccz .LBB0_2\n"
+            + LOAD + ".LBB0_2:\n\ts_andn2_b64 vcc, exec, s[12:13]\n\ts_cbranch_vccz .LBB0_3\n"
+            "\tv_readfirstlane_b32 s6, v10\n.LBB0_3:\n\ts_waitcnt vmcnt(0)\n")
+    assert _hazards(body)
+
+
+def test_flag_set_to_a_constant_is_known():
+    # F = -1; if (c) { F = 0; load }; if (F) { use }: the use never follows the load
+    body = ("\ts_mov_b64 s[12:13], -1\n\ts_cbranch_scc1 .LBB0_2\n\ts_mov_b64 s[12:13], 0\n" + LOAD +
+            ".LBB0_2:\n\ts_and_b64 vcc, exec, s[12:13]\n\ts_cbranch_vccz .LBB0_3\n"
+            "\tv_readfirstlane_b32 s6, v10\n.LBB0_3:\n\ts_waitcnt vmcnt(0)\n")
+    assert not _hazards(body)
+    assert _hazards(body.replace("s_mov_b64 s[12:13], 0\n", "s_mov_b64 s[12:13], s[4:5]\n"))
+    # the flag written in between by something else: both directions again
+    body_w = body.replace(".LBB0_2:\n", ".LBB0_2:\n\ts_cselect_b64 s[12:13], -1, 0\n")
+    assert _hazards(body_w)
+    # the other constant: the use follows the load
+    assert _hazards(body.replace("s_mov_b64 s[12:13], 0\n", "s_mov_b64 s[12:13], -1\n", 1).replace(
+        "\ts_mov_b64 s[12:13], -1\n\ts_cbranch_scc1", "\ts_mov_b64 s[12:13], 0\n\ts_cbranch_scc1"))
