@@ -814,18 +814,20 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // keep this order (the compiler would otherwise gather the vector work
     // after the last MFMA and reorder the MFMAs, collapsing the read-ahead);
     // an empty use pins each pair in its group.
-    auto phase_a = [&](int kb, const f32x16 (&sc)[2], f32x16 (&sn)[2], bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+    // The first three K operands (kf, read by the caller before the step's
+    // scalar work so that their latency overlaps it) and, in the last three
+    // groups, the first three V operands of phase B (vf).
+    auto phase_a = [&](int kb, int vb, bf16x8 (&kf)[3], bf16x8 (&vf)[3], const f32x16 (&sc)[2], f32x16 (&sn)[2],
+                       bf16x8 (&pb)[4]) __attribute__((always_inline)) {
       constexpr int N = 2 * KS;
       constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
       uint32_t w[16];
-      bf16x8 kf[3];
-#pragma unroll
-      for (int i = 0; i < 3; ++i) kf[i] = rdk(kb, i);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < N; ++i) {
         sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? mneg : sn[i & 1], 0, 0, 0);
         if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
+        else vf[i + 3 - N] = rdv(vb, i + 3 - N);
         copies_a(i);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
@@ -878,18 +880,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       l_run += ls[0] + ls[1];
     };
     // Phase B of a step: O^T += V^T P^T from the stage at vb (operand reads
-    // three ahead), in groups like phase A's, with the row sums of P (first)
-    // and the row maximum of the next scores sn (already masked; last, so that
-    // the last MFMAs of phase A have completed); returns the maximum relative
-    // to the base.
-    auto phase_b = [&](int vb, const bf16x8 (&pb)[4], const f32x16 (&sn)[2]) __attribute__((always_inline)) -> float {
+    // three ahead), in groups like phase A's: the row sums of P in the first
+    // half of the groups, the row maximum of the next scores sn (already
+    // masked) in the second half, when the last MFMAs of phase A, which wrote
+    // sn, have long completed; returns the maximum relative to the base.
+    // (vf: the first three V operands, read in phase A)
+    auto phase_b = [&](int vb, bf16x8 (&vf)[3], const bf16x8 (&pb)[4], const f32x16 (&sn)[2])
+        __attribute__((always_inline)) -> float {
       constexpr int N = 4 * DT;
-      constexpr int PER = 16 / N;   // sums and max3 operations per MFMA
+      constexpr int PER = 32 / N;   // sums (first half) or max3 operations (second half) per MFMA
       float x[2] = {-INFINITY, -INFINITY};
       float ls[2] = {0.f, 0.f};
-      bf16x8 vf[3];
-#pragma unroll
-      for (int i = 0; i < 3; ++i) vf[i] = rdv(vb, i);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < N; ++i) {
@@ -898,13 +899,15 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         copies_b(i, false);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
-          const int q = i * PER + u;
-          sum_pair(__builtin_bit_cast(u32x4, pb[q >> 2])[q & 3], ls[q & 1]);
-          asm volatile("" :: "v"(ls[q & 1]));
-          // the max starts two groups late; the first pairs go with the end
-          const int qm = (q + 2) % 16, h = qm & 1, e = (qm >> 1) * 2;
-          x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
-          asm volatile("" :: "v"(x[h]));
+          if (i < N / 2) {
+            const int q = i * PER + u;
+            sum_pair(__builtin_bit_cast(u32x4, pb[q >> 2])[q & 3], ls[q & 1]);
+            asm volatile("" :: "v"(ls[q & 1]));
+          } else {
+            const int q = (i - N / 2) * PER + u, h = q & 1, e = (q >> 1) * 2;
+            x[h] = fmaxf(fmaxf(x[h], sn[h][e]), sn[h][e + 1]);
+            asm volatile("" :: "v"(x[h]));
+          }
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -955,13 +958,16 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     };
     // Step j < nsteps - 1 at ring position p: current S in sc, next S into sn.
     auto step = [&](int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
+      bf16x8 kf[3], vf[3];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) kf[i] = rdk(kbase(p + 1), i);
       if (j == touch_at) touch_q();
       const bool direct = issue(p + kAhead, true);
       rebase(sc);
       bf16x8 pb[4];
-      phase_a(kbase(p + 1), sc, sn, pb);
+      phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, pb);
       if (j + 1 >= n_full) mask(sn, (kbeg + j + 1) * kKv);
-      mx = phase_b(vbase(p), pb, sn);
+      mx = phase_b(vbase(p), vf, pb, sn);
       step_barrier(direct);
       ++p;
     };
