@@ -237,12 +237,15 @@ def question_only_point(seed: int, stream):
     return res
 
 
-def config_points(seed: int, stream, names=("llama8b-single", "topk10-f0.6", "llama70b-long-high")) -> dict:
+def config_points(seed: int, stream, names=("llama8b-single", "topk10-f0.0", "topk10-f0.6", "llama70b-long-high",
+                                           "llama70b-long-low")) -> dict:
     """Attention time of the other configurations (not the headline): the
-    single 8B-shaped request, the top-k sweep at 60 % cached blocks and the
-    70B-shaped long-context batch in trie order (high hit). Each batch is
-    materialised on the GPU, its suffix appended, then the attention call is
-    timed with HIP events (median of several calls after a warm-up)."""
+    single 8B-shaped request, the top-k sweep at 0 % and 60 % cached blocks and
+    the 70B-shaped long-context batch in trie order (high hit) and retrieval
+    order (low hit). Each batch is materialised on the GPU, its suffix
+    appended, then the attention call is timed with HIP events (median of
+    several calls after calls for SETTLE_S seconds, so that the clock has
+    settled under this batch's load)."""
     import torch
     from paper_2606_19667_amd import batch as B
     from paper_2606_19667_amd import cw
@@ -258,8 +261,10 @@ def config_points(seed: int, stream, names=("llama8b-single", "topk10-f0.6", "ll
         fl = attention_flops(P, S, hq, D)
         fn = lambda: cw.suffix_prefill_attn(db.meta, db.q, db.k_cache, db.v_cache, db.scale, out=out, stream=stream)
         n = max(3, min(50, int(2e12 / fl)))
-        for _ in range(max(2, n // 5)):
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 3 * SETTLE_S:
             fn()
+            torch.cuda.synchronize()
         t = percentiles_us(timed_calls(fn, stream, n))
         sec = t["median"] * 1e-6
         out_all[name] = {"attention_us": t, "GFLOP": round(fl / 1e9, 3),

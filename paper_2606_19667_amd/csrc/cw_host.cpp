@@ -566,12 +566,14 @@ extern "C" cw_status cw_release_batch(cw_pool* pool, const int32_t* block_table,
 // grid is persistent, one workgroup per CU; workgroup w runs entries w,
 // w + grid, w + 2 grid, ... of its queue.
 //
-// Queues are filled longest-processing-time first (each entry, heaviest first,
-// goes to the queue with the least work so far), so the queues end together.
 // With enough (request, KV head) pairs and 256 queues, the pairs are first
 // spread over the eight L2 partitions (queue w runs on partition w % 8) by
-// total work, so every tile re-reading a pair's K/V hits that partition's L2;
-// the entries of a partition then fill its 32 queues.
+// total work, so that every tile re-reading a pair's K/V does so from that
+// partition's L2; the entries of a partition then fill its 32 queues in
+// rounds of one entry per queue in pair order (see rounds()), so that the
+// tiles running together share their K/V. Otherwise queues are filled
+// longest-processing-time first (each entry, heaviest first, goes to the
+// queue with the least work so far), so that they end together.
 // ---------------------------------------------------------------------------
 namespace {
 
@@ -651,6 +653,53 @@ void lpt(const std::vector<Entry>& ents, std::vector<int32_t> idx, const std::ve
   }
 }
 
+// Rounds over the queues of one L2 partition: the entries, ordered by
+// (request, KV head) pair, split run and first row, are cut into rounds of one
+// entry per queue, and within a round the heaviest entry goes to the queue
+// with the least work so far. The queues run a round at about the same time,
+// so the tiles that run together on the partition come from one or two pairs
+// and read the same K/V blocks out of its L2. The last three rounds' worth of
+// entries go longest first to the least-loaded queue, so that the queues end
+// together.
+void rounds(const std::vector<Entry>& ents, std::vector<int32_t> idx, const std::vector<int32_t>& queues,
+            std::vector<std::vector<int32_t>>* q) {
+  std::stable_sort(idx.begin(), idx.end(), [&](int32_t a, int32_t b) {
+    const Entry& x = ents[size_t(a)];
+    const Entry& y = ents[size_t(b)];
+    if (x.pair != y.pair) return x.pair < y.pair;
+    if (x.f[cw::kEntSplit] != y.f[cw::kEntSplit]) return x.f[cw::kEntSplit] < y.f[cw::kEntSplit];
+    return x.f[cw::kEntRow0] < y.f[cw::kEntRow0];
+  });
+  const size_t nq = queues.size();
+  std::vector<int64_t> load(nq, 0);
+  std::vector<size_t> order(nq);
+  // the last kTail rounds' entries are placed longest first instead, which
+  // evens out the queues' ends
+  constexpr size_t kTail = 3;
+  const size_t n_rounds = idx.size() > kTail * nq ? (idx.size() - kTail * nq) / nq : 0;
+  for (size_t r0 = 0; r0 < n_rounds * nq; r0 += nq) {
+    std::vector<int32_t> round(idx.begin() + std::ptrdiff_t(r0), idx.begin() + std::ptrdiff_t(r0 + nq));
+    std::stable_sort(round.begin(), round.end(),
+                     [&](int32_t a, int32_t b) { return ents[size_t(a)].cost > ents[size_t(b)].cost; });
+    std::iota(order.begin(), order.end(), size_t(0));
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return load[a] < load[b]; });
+    for (size_t k = 0; k < round.size(); ++k) {
+      load[order[k]] += ents[size_t(round[k])].cost;
+      (*q)[size_t(queues[order[k]])].push_back(round[k]);
+    }
+  }
+  std::vector<int32_t> tail(idx.begin() + std::ptrdiff_t(n_rounds * nq), idx.end());
+  std::stable_sort(tail.begin(), tail.end(),
+                   [&](int32_t a, int32_t b) { return ents[size_t(a)].cost > ents[size_t(b)].cost; });
+  for (int32_t i : tail) {
+    size_t x = 0;
+    for (size_t k = 1; k < nq; ++k)
+      if (load[k] < load[x]) x = k;
+    load[x] += ents[size_t(i)].cost;
+    (*q)[size_t(queues[x])].push_back(i);
+  }
+}
+
 Queues plan_queues(const std::vector<Entry>& ents, int32_t batch, int32_t hkv) {
   Queues qs;
   qs.grid = int32_t(std::min<size_t>(ents.size(), cw::kNumCu));
@@ -687,7 +736,7 @@ Queues plan_queues(const std::vector<Entry>& ents, int32_t batch, int32_t hkv) {
         for (int32_t i : all)
           if (part[size_t(ents[size_t(i)].pair)] == x) idx.push_back(i);
         for (int32_t w = x; w < qs.grid; w += cw::kNumXcd) queues.push_back(w);
-        lpt(ents, idx, queues, &qs.q);
+        rounds(ents, idx, queues, &qs.q);
       }
     }
   }

@@ -238,24 +238,62 @@ def test_plan_covers_every_row_and_step_once(shape):
             assert plan[cw.HDR_GRID] == min(256, len(ents))
 
 
+def _queue_loads(plan):
+    load, heavy = {}, 0
+    for w, i, e in _entries(plan):
+        c = int(e[cw.ENT_KEND] - e[cw.ENT_KBEG]) + 1
+        load[w] = load.get(w, 0) + c
+        heavy = max(heavy, c)
+    return load, heavy
+
+
 def test_plan_queues_are_balanced_longest_first():
-    """Each queue runs its entries heaviest first, and no queue carries more
-    than the lightest queue plus its heaviest entry (list scheduling)."""
+    """Without partition grouping (fewer than 32 pairs), each queue runs its
+    entries heaviest first, and no queue carries more than the lightest queue
+    plus its heaviest entry (list scheduling)."""
     rng = np.random.default_rng(5)
-    S = rng.integers(1, 1400, size=16)
-    P = rng.integers(0, 20, size=16) * 64
+    S = rng.integers(1, 1400, size=3)
+    P = rng.integers(0, 20, size=3) * 64
     cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
     plan = cw.suffix_prefill_plan(cu, P, 32, 8, 128)
-    load, heavy = {}, {}
+    assert not _grouped(plan)
     last = {}
     for w, i, e in _entries(plan):
         c = int(e[cw.ENT_KEND] - e[cw.ENT_KBEG]) + 1
         assert c <= last.get(w, 1 << 30)
         last[w] = c
-        load[w] = load.get(w, 0) + c
-        heavy[w] = max(heavy.get(w, 0), c)
-    assert len(load) == 256
-    assert max(load.values()) <= min(load.values()) + max(heavy.values())
+    load, heavy = _queue_loads(plan)
+    assert max(load.values()) <= min(load.values()) + heavy
+
+
+def test_grouped_plan_runs_rounds_in_pair_order_and_stays_balanced():
+    """With partition grouping, the entries a partition's queues hold at one
+    queue position (a round, run at about the same time) are consecutive in
+    (pair, split run, first row) order, rounds follow each other in that
+    order, and the queues stay balanced within one entry's work."""
+    rng = np.random.default_rng(5)
+    S = rng.integers(1, 1400, size=16)
+    P = rng.integers(0, 20, size=16) * 64
+    cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
+    for hkv, splits in ((8, 1), (4, 1), (8, 2)):
+        plan = cw.suffix_prefill_plan(cu, P, 32, hkv, 128, splits)
+        assert _grouped(plan)
+        qlen = int(plan[cw.HDR_QUEUE_LEN])
+        for x in range(8):
+            rounds = []
+            for i in range(qlen):
+                keys = sorted((int(e[0]) * hkv + int(e[1]), int(e[cw.ENT_SPLIT]), int(e[cw.ENT_ROW0]))
+                              for w, j, e in _entries(plan) if w % 8 == x and j == i)
+                if keys:
+                    rounds.append(keys)
+            # all but the last three rounds (placed longest first) are runs of
+            # the sorted order, one after another
+            body = rounds[:-3]
+            flat = [k for r in body for k in r]
+            assert flat == sorted(flat)
+            assert all(len(r) == 32 for r in body)
+        load, heavy = _queue_loads(plan)
+        assert max(load.values()) <= min(load.values()) + heavy
 
 
 @pytest.mark.parametrize("grouped", [False, True])
@@ -288,9 +326,9 @@ def test_plan_groups_pairs_on_one_partition():
 
 
 def test_plan_check_words_bind_entries_to_the_batch():
-    """Each entry's check word is the library's hash of its fields seeded with
-    the batch fingerprint: plans of two batches that differ in one prefix
-    length differ in every real entry's check word."""
+    """Each entry's check word derives from the batch fingerprint and the
+    entry's position: plans of two batches that differ in one prefix length
+    differ in every real entry's check word."""
     cu = np.array([0, 300, 900], np.int32)
     a = cw.suffix_prefill_plan(cu, [0, 64], 32, 8, 128)
     b = cw.suffix_prefill_plan(cu, [0, 80], 32, 8, 128)
