@@ -602,7 +602,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 
   // Raw Q (bf16) of the entry to come, loaded before the first steps for the
   // first entry and during an entry's last step for the next one, so that an
-  // entry starts without waiting for its queries (unsplit kernel only).
+  // entry starts without waiting for its queries.
   u32x4 qn[KS];
   // Plan entry words of the entry to come and of the one after it, one word
   // per lane: lane l holds word l % 16 of entry e (l % 32 < 16) or of entry
@@ -638,7 +638,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // the wait that completes the words (and the table word loaded before),
   // tied to the register that receives them
   asm volatile("s_waitcnt vmcnt(0)" : "+v"(desc) :: "memory");
-  if (!SPLIT) load_q(q_source(desc, false, true));
+  load_q(q_source(desc, false, true));
   // the first call below reads the table word: complete since the wait above
 
   // ---- first steps of the queue
@@ -670,9 +670,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     if (desc_word(dw, false, cw::kEntR) < 0 ||
         uint32_t(desc_word(dw, false, cw::kEntCheck)) != cw::entry_tag(a.fp_lo, a.fp_hi, uint32_t(e)))
       break;
-    // where the next entry's Q comes from (the split kernel has no registers
-    // to spare for a prefetch)
-    const u32x4* q_next = SPLIT ? nullptr : q_source(dw, true, e + grid < a.num_entries);
+    // where the next entry's Q comes from
+    const u32x4* q_next = q_source(dw, true, e + grid < a.num_entries);
     const int g = desc_word(dw, false, cw::kEntG), row0 = desc_word(dw, false, cw::kEntRow0);
     const int nvalid = desc_word(dw, false, cw::kEntNvalid), P = desc_word(dw, false, cw::kEntP);
     const int qrow0 = desc_word(dw, false, cw::kEntQrow);
@@ -698,24 +697,18 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
             *reinterpret_cast<f32x4*>(po + t * 32 + gq * 8 + half * 4) = f32x4{0.f, 0.f, 0.f, 0.f};
         if (half == 0) a.part_lse[prow] = -INFINITY;
       }
-      // the next entry's words, waited for here (this entry has no last step)
+      // the next entry's Q and words, waited for here (this entry has no
+      // last step)
+      load_q(q_next);
       load_desc(e + grid);
       __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       continue;
     }
 
     bf16x8 qf[KS];
-    if constexpr (SPLIT) {
-      if (row_ok) {
-        const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (qrow * a.hq + head) * D);
-#pragma unroll
-        for (int s = 0; s < KS; ++s) qf[s] = scale_bf16x8(qp[2 * s + half], a.c_log2);
-      } else {
-#pragma unroll
-        for (int s = 0; s < KS; ++s) qf[s] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
-      }
-    } else {
-      // qn landed before the last step barrier (or the first steps' wait)
+    {
+      // qn landed before the last step barrier (or the first steps' wait, or
+      // an empty run's wait)
 #pragma unroll
       for (int s = 0; s < KS; ++s) asm volatile("" : "+v"(qn[s]));
 #pragma unroll
@@ -795,9 +788,10 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // phase A, the second half likewise in phase B; a step without phase A
     // (an entry's last) puts all of them in phase B.
     constexpr int HALF_C = LPW / 2;
+    constexpr int kEarly = 2;   // phase A groups issued before a step's copy work
     auto copies_a = [&](int i) __attribute__((always_inline)) {
       constexpr int E = 2 * KS / HALF_C;
-      if (i % E == 0) copy_part(i / E);
+      if (i % E == kEarly) copy_part(i / E);
     };
     auto copies_b = [&](int i, bool all) __attribute__((always_inline)) {
       constexpr int E = 4 * DT / HALF_C, EA = 4 * DT / LPW;
@@ -817,14 +811,16 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // The first three K operands (kf, read by the caller before the step's
     // scalar work so that their latency overlaps it) and, in the last three
     // groups, the first three V operands of phase B (vf).
+    // Groups [i0, i1) of phase A (a step issues the first groups before its
+    // scalar copy work, so that the matrix pipe has work meanwhile); pack
+    // ends the phase.
     auto phase_a = [&](int kb, int vb, bf16x8 (&kf)[3], bf16x8 (&vf)[3], const f32x16 (&sc)[2], f32x16 (&sn)[2],
-                       bf16x8 (&pb)[4]) __attribute__((always_inline)) {
+                       uint32_t (&w)[16], bf16x8 (&pb)[4], int i0, int i1, bool pack) __attribute__((always_inline)) {
       constexpr int N = 2 * KS;
       constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
-      uint32_t w[16];
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < N; ++i) {
+      for (int i = i0; i < i1; ++i) {
         sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? mneg : sn[i & 1], 0, 0, 0);
         if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
         else vf[i + 3 - N] = rdv(vb, i + 3 - N);
@@ -836,7 +832,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      pack_pb(w, pb);
+      if (pack) pack_pb(w, pb);
     };
     // The last step of an entry (no next scores): O^T += V^T P^T with the
     // probabilities of 16-key slice kk + 1 formed while the PV MFMAs of slice
@@ -952,7 +948,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // Two steps before its last one, an entry brings the next entry's queries
     // into L2 (one 128-byte line per lane), so that their load at the last
     // step does not wait for HBM. (Entries of one or two steps skip it.)
-    const int touch_at = SPLIT ? -1 : last - 2;
+    const int touch_at = last - 2;
     auto touch_q = [&]() __attribute__((always_inline)) {
       touch_line(reinterpret_cast<const uint8_t*>(q_next) + half * 128, own_area);
     };
@@ -962,10 +958,12 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 3; ++i) kf[i] = rdk(kbase(p + 1), i);
       if (j == touch_at) touch_q();
-      const bool direct = issue(p + kAhead, true);
       rebase(sc);
       bf16x8 pb[4];
-      phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, pb);
+      uint32_t w[16];
+      phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, 0, kEarly, false);
+      const bool direct = issue(p + kAhead, true);
+      phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, kEarly, 2 * KS, true);
       if (j + 1 >= n_full) mask(sn, (kbeg + j + 1) * kKv);
       mx = phase_b(vbase(p), vf, pb, sn);
       step_barrier(direct);
@@ -986,7 +984,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     {   // the entry's last step: P and PV only. qf is no longer needed: the
         // next entry's Q is loaded now, ahead of this step's table word and
         // copies, so that this step's barrier completes it.
-      if (!SPLIT) load_q(q_next);
+      load_q(q_next);
       load_desc(e + grid);
       const bool direct = issue(p + kAhead, true);
       rebase(sa);
