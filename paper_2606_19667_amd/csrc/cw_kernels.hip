@@ -106,6 +106,45 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 
   const int nch = D / 8;   // 16-byte chunks per row and head
   const int64_t src0 = int64_t(cu0 + j0) * hkv * nch;
+  // V: the cache holds each block transposed, [blk][head][d][slot]. A task is
+  // (head, 8 values of d, 8 slots): it loads the 8 slots' 16-byte chunks,
+  // transposes the 8 x 8 block of bfloat16 in registers (v_perm) and stores 8
+  // rows of 8 slots. Slots past the unit's rows are neither read (the row index
+  // is clamped) nor written. The loads of a thread's first task are issued
+  // before the K loads, so that both are in flight together.
+  uint16_t* vd = v_cache + int64_t(blk) * hkv * D * kBs;
+  const int ntask = hkv * nch * 2;
+  uint32_t rw[8][4];                   // rw[k][j]: slot 8 sh + k, d pair j
+  auto v_load = [&](int u) {
+    const int sh = u & 1, dc = (u >> 1) % nch, h = (u >> 1) / nch;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int slot = min(8 * sh + k, nv - 1);
+      const u32x4 x = v_new[src0 + (int64_t(slot) * hkv + h) * nch + dc];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rw[k][j] = x[j];
+    }
+  };
+  auto v_store = [&](int u) {
+    const int sh = u & 1, dc = (u >> 1) % nch, h = (u >> 1) / nch;
+    const int nvs = min(8, nv - 8 * sh);   // valid slots of this task
+    uint16_t* dst = vd + (int64_t(h) * D + 8 * dc) * kBs + 8 * sh;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {      // output row d = 8 dc + e: 8 slots
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
+      uint32_t o[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = __builtin_amdgcn_perm(rw[2 * k + 1][e >> 1], rw[2 * k][e >> 1], sel);
+      if (nvs == 8) {
+        *reinterpret_cast<u32x4*>(dst + e * kBs) = u32x4{o[0], o[1], o[2], o[3]};
+      } else {
+        for (int k = 0; k < nvs; ++k) dst[e * kBs + k] = uint16_t(o[k >> 1] >> (16 * (k & 1)));
+      }
+    }
+  };
+  // a task whose slots all lie past the unit's rows has nothing to do
+  auto v_active = [&](int u) { return u < ntask && 8 * (u & 1) < nv; };
+  if (v_active(tid)) v_load(tid);
   // K: source chunk c = (slot, head, chunk) -> cache [blk][head][slot][chunk].
   // A thread issues all loads of a batch before its stores.
   u32x4* kd = k_cache + int64_t(blk) * hkv * kBs * nch;
@@ -125,40 +164,11 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
       }
     }
   }
-  // V: the cache holds each block transposed, [blk][head][d][slot]. A task is
-  // (head, 8 values of d, 8 slots): it loads the 8 slots' 16-byte chunks,
-  // transposes the 8 x 8 block of bfloat16 in registers (v_perm) and stores 8
-  // rows of 8 slots. Slots past the unit's rows are neither read (the row index
-  // is clamped) nor written.
-  uint16_t* vd = v_cache + int64_t(blk) * hkv * D * kBs;
-  const int ntask = hkv * nch * 2;
-  for (int u = tid; u < ntask; u += kThreads) {
-    const int sh = u & 1;              // slots 8 sh .. 8 sh + 7
-    const int dc = (u >> 1) % nch;     // d = 8 dc .. 8 dc + 7
-    const int h = (u >> 1) / nch;
-    const int nvs = min(8, nv - 8 * sh);   // valid slots of this task
-    if (nvs <= 0) continue;
-    uint32_t rw[8][4];                 // rw[k][j]: slot 8 sh + k, d pair j
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int slot = min(8 * sh + k, nv - 1);
-      const u32x4 x = v_new[src0 + (int64_t(slot) * hkv + h) * nch + dc];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) rw[k][j] = x[j];
-    }
-    uint16_t* dst = vd + (int64_t(h) * D + 8 * dc) * kBs + 8 * sh;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {      // output row d = 8 dc + e: 8 slots
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
-      uint32_t o[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) o[k] = __builtin_amdgcn_perm(rw[2 * k + 1][e >> 1], rw[2 * k][e >> 1], sel);
-      if (nvs == 8) {
-        *reinterpret_cast<u32x4*>(dst + e * kBs) = u32x4{o[0], o[1], o[2], o[3]};
-      } else {
-        for (int k = 0; k < nvs; ++k) dst[e * kBs + k] = uint16_t(o[k >> 1] >> (16 * (k & 1)));
-      }
-    }
+  if (v_active(tid)) v_store(tid);
+  for (int u = tid + kThreads; u < ntask; u += kThreads) {
+    if (!v_active(u)) continue;
+    v_load(u);
+    v_store(u);
   }
 }
 
