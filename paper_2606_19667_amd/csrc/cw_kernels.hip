@@ -5,10 +5,11 @@
 // suffix tokens are prefilled; they attend causally over themselves and fully
 // over the prefix, whose K/V the engine keeps in fixed-size blocks.
 //
-// Attention kernel design (one workgroup = 8 wavefronts, two per SIMD = one tile):
-//  * A tile is (request r, KV head g, a run of T suffix rows); its 256 MFMA
-//    rows pack the G = Hq/Hkv query heads of g over T = 256/G positions, so
-//    every K/V byte staged in LDS serves all heads of the group.
+// Attention kernel design (persistent workgroups of 8 wavefronts, two per SIMD):
+//  * A plan entry is (request r, KV head g, a run of T suffix rows, a run of
+//    64-key steps); its 256 MFMA rows pack the G = Hq/Hkv query heads of g
+//    over T = 256/G positions, so every K/V byte staged in LDS serves all
+//    heads of the group. Workgroup w runs entries w, w + grid, ...
 //  * Each wave owns 32 packed rows and computes S^T = K Q^T with
 //    v_mfma_f32_32x32x16_bf16: in the 32x32 accumulator layout a lane then
 //    holds one query column and 16 keys, so row max / sum need one exchange
@@ -16,7 +17,8 @@
 //  * O^T = V^T P^T uses the packed probabilities directly as the B operand;
 //    the cache keeps each V block transposed, so V operands are plain reads.
 //  * K/V steps of 64 keys (4 blocks) are copied from the cache into a ring of
-//    three LDS stages by load-to-LDS instructions, two to three steps ahead.
+//    four LDS stages by load-to-LDS instructions three steps ahead, by a copy
+//    cursor that runs across entry boundaries.
 //  * Softmax in fp32 and base 2 with a lazily moved base; only steps that
 //    cross the causal diagonal apply the mask; keys past the prompt end are
 //    zero-filled so stale cache bytes never reach the result.
