@@ -319,7 +319,7 @@ def qkv_projection_point(w, seed: int, stream, hidden: int = 4096, rope_base: fl
     x = inputs.normal_bf16((seed, 101), (T, hidden), "cuda")
     wt = inputs.scaled_normal_bf16((seed, 102), (nf, hidden), hidden ** -0.5, "cuda")
     kc = torch.zeros((s.num_blocks, hkv, 16, D), dtype=torch.bfloat16, device="cuda")
-    vc = torch.zeros((s.num_blocks, hkv, D, 16), dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros((s.num_blocks, hkv, 16, D), dtype=torch.bfloat16, device="cuda")
     n_pos = int((s.prefix_len + np.diff(s.cu_suffix)).max())
     rope = torch.from_numpy(cw.rope_table(n_pos, D, rope_base)).cuda()
     q = torch.empty((T, hq, D), dtype=torch.bfloat16, device="cuda")

@@ -25,8 +25,7 @@
  *      q, out        [total_s, Hq, D]        suffix rows of all requests, request-major
  *      k_new, v_new  [total_s, Hkv, D]
  *      k_cache       [num_blocks, Hkv, block_size, D]   block rows are tokens
- *      v_cache       [num_blocks, Hkv, D, block_size]   each block transposed: rows are
- *                    head dimensions, so 16 bytes hold 8 consecutive tokens of one d
+ *      v_cache       [num_blocks, Hkv, block_size, D]   the same
  *      block_table   int32 [batch, bt_stride]; row r lists the physical blocks of
  *                    request r's logical blocks 0 .. ceil(L_r / block_size) - 1
  *      cu_suffix     int32 [batch + 1]; request r owns rows cu[r] .. cu[r+1]-1,
@@ -54,7 +53,7 @@ typedef int32_t cw_status;
 #define CW_ENOSPC (-3)       /* block pool exhausted */
 #define CW_EHIP (-4)         /* a HIP runtime call or kernel launch failed */
 
-#define CW_ABI_VERSION 3
+#define CW_ABI_VERSION 4
 
 /* ABI version of the loaded library (CW_ABI_VERSION at build time). */
 int32_t cw_abi_version(void);
@@ -228,7 +227,7 @@ cw_status cw_tree_order(const cw_tree* tree, int32_t strategy, const int64_t* do
  *
  * For every request r and token t in [P_r, L_r):
  *   k_cache[block_table[r, t / bs], h, t % bs, :] = k_new[cu[r] + t - P_r, h, :]
- *   v_cache[block_table[r, t / bs], h, :, t % bs] = v_new[cu[r] + t - P_r, h, :]
+ *   v_cache[block_table[r, t / bs], h, t % bs, :] = v_new[cu[r] + t - P_r, h, :]
  * a bit copy. Nothing else in the caches changes. A table entry outside
  * [0, num_blocks) drops the writes of its tokens (never a fault).
  *   cu_suffix_dev / prefix_len_dev   device copies read by the kernel
@@ -413,7 +412,7 @@ cw_status cw_rope_table(int32_t n_positions, int32_t head_dim, double base, floa
  *   rot(u)[j]         = u[j] cos(p th_j) - u[j + D/2] sin(p th_j)
  *   rot(u)[j + D/2]   = u[j + D/2] cos(p th_j) + u[j] sin(p th_j),  j < D/2
  *   q_out[t][h][:]    = rot(y_q of head h)
- *   k_cache[blk][g][p % 16][:], v_cache[blk][g][:][p % 16] = rot(y_k), y_v
+ *   k_cache[blk][g][p % 16][:], v_cache[blk][g][p % 16][:] = rot(y_k), y_v
  *     of KV head g, blk = block_table[r][p / 16]; a block id outside
  *     [0, num_blocks) is skipped (nothing written).
  * Every output is rounded once, RNE, to bf16; every other cache byte keeps

@@ -108,7 +108,7 @@ def materialize(w: Workload, device="cuda", keep_host=None, gen_device=None,
     k_cache = torch.full((sched.num_blocks, hkv, bs, D), 0, dtype=torch.int16, device=device)
     k_cache.fill_(SENTINEL_BITS)
     k_cache = k_cache.view(torch.bfloat16)
-    v_cache = k_cache.clone().view(sched.num_blocks, hkv, D, bs)   # blocks stored [d][slot]
+    v_cache = k_cache.clone()
     total = int(sched.cu_suffix[-1])
     q = torch.empty((total, hq, D), dtype=torch.bfloat16, device=device)
     k_new = torch.empty((total, hkv, D), dtype=torch.bfloat16, device=device)
@@ -126,7 +126,7 @@ def materialize(w: Workload, device="cuda", keep_host=None, gen_device=None,
         if nblk:
             ids = torch.from_numpy(sched.block_table[r, :nblk].astype(np.int64)).to(device)
             k_cache[ids] = _blocks_view(k[:P], bs).to(device)
-            v_cache[ids] = _blocks_view(v[:P], bs).transpose(2, 3).to(device)
+            v_cache[ids] = _blocks_view(v[:P], bs).to(device)
         if r in keep:
             lk[r], lv[r], qh[r] = k.cpu(), v.cpu(), qs.cpu()
     meta = cw.BatchMeta(sched.block_table, sched.cu_suffix, sched.prefix_len, hq, hkv, D, device)

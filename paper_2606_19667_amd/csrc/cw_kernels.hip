@@ -15,7 +15,7 @@
 //    holds one query column and 16 keys, so row max / sum need one exchange
 //    with lane ^ 32 and the softmax state is lane-local.
 //  * O^T = V^T P^T uses the packed probabilities directly as the B operand;
-//    the cache keeps each V block transposed, so V operands are plain reads.
+//    its V^T operand comes from token-major V by transposing LDS reads.
 //  * K/V steps of 64 keys (4 blocks) are copied from the cache into a ring of
 //    four LDS stages by load-to-LDS instructions three steps ahead, by a copy
 //    cursor that runs across entry boundaries.
@@ -47,6 +47,7 @@ constexpr int kKv = cw::kKvTile;
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // Two floats to two bfloat16 (round to nearest even) in one dword, low first.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -58,14 +59,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // contributes ceil(S_r / 16) units, unit j covering suffix rows 16 j ..
 // min(16 j + 16, S_r) - 1, which (P_r being a multiple of 16) fill slots
 // 0 .. of a single cache block. One workgroup per unit finds its (request,
-// unit) with a wave-wide prefix sum over the per-request unit counts, copies
-// the K rows ([slot][d] in the cache, contiguous 16-byte chunks) and writes V
-// transposed ([d][slot]) by 8 x 8 register transposes: 16-byte stores per
-// 8-slot half row, one element per slot where a partial block ends.
+// unit) with a wave-wide prefix sum over the per-request unit counts and
+// copies the K and V rows ([slot][d] in both caches) in 16-byte chunks.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(
     const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_cache,
-    uint16_t* __restrict__ v_cache, const int32_t* __restrict__ bt, int bt_stride,
+    u32x4* __restrict__ v_cache, const int32_t* __restrict__ bt, int bt_stride,
     const int32_t* __restrict__ cu, const int32_t* __restrict__ plen, int batch, int hkv, int D,
     int num_blocks) {
   __shared__ int s_unit[2];
@@ -106,71 +105,33 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
   const int blk = bt[int64_t(r) * bt_stride + t0 / kBs];
   if (nv <= 0 || blk < 0 || blk >= num_blocks) return;
 
+  // Source chunk c = (slot, head, chunk) of either tensor goes to cache
+  // [blk][head][slot][chunk]. A thread issues all loads of a batch (K and V)
+  // before its stores.
   const int nch = D / 8;   // 16-byte chunks per row and head
   const int64_t src0 = int64_t(cu0 + j0) * hkv * nch;
-  // V: the cache holds each block transposed, [blk][head][d][slot]. A task is
-  // (head, 8 values of d, 8 slots): it loads the 8 slots' 16-byte chunks,
-  // transposes the 8 x 8 block of bfloat16 in registers (v_perm) and stores 8
-  // rows of 8 slots. Slots past the unit's rows are neither read (the row index
-  // is clamped) nor written. The loads of a thread's first task are issued
-  // before the K loads, so that both are in flight together.
-  uint16_t* vd = v_cache + int64_t(blk) * hkv * D * kBs;
-  const int ntask = hkv * nch * 2;
-  uint32_t rw[8][4];                   // rw[k][j]: slot 8 sh + k, d pair j
-  auto v_load = [&](int u) {
-    const int sh = u & 1, dc = (u >> 1) % nch, h = (u >> 1) / nch;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int slot = min(8 * sh + k, nv - 1);
-      const u32x4 x = v_new[src0 + (int64_t(slot) * hkv + h) * nch + dc];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) rw[k][j] = x[j];
-    }
-  };
-  auto v_store = [&](int u) {
-    const int sh = u & 1, dc = (u >> 1) % nch, h = (u >> 1) / nch;
-    const int nvs = min(8, nv - 8 * sh);   // valid slots of this task
-    uint16_t* dst = vd + (int64_t(h) * D + 8 * dc) * kBs + 8 * sh;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {      // output row d = 8 dc + e: 8 slots
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
-      uint32_t o[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) o[k] = __builtin_amdgcn_perm(rw[2 * k + 1][e >> 1], rw[2 * k][e >> 1], sel);
-      if (nvs == 8) {
-        *reinterpret_cast<u32x4*>(dst + e * kBs) = u32x4{o[0], o[1], o[2], o[3]};
-      } else {
-        for (int k = 0; k < nvs; ++k) dst[e * kBs + k] = uint16_t(o[k >> 1] >> (16 * (k & 1)));
-      }
-    }
-  };
-  // a task whose slots all lie past the unit's rows has nothing to do
-  auto v_active = [&](int u) { return u < ntask && 8 * (u & 1) < nv; };
-  if (v_active(tid)) v_load(tid);
-  // K: source chunk c = (slot, head, chunk) -> cache [blk][head][slot][chunk].
-  // A thread issues all loads of a batch before its stores.
-  u32x4* kd = k_cache + int64_t(blk) * hkv * kBs * nch;
+  const int64_t dst0 = int64_t(blk) * hkv * kBs * nch;
   const int nk = nv * hkv * nch;
   constexpr int kBatch = 8;
   for (int c0 = tid; c0 < nk; c0 += kThreads * kBatch) {
-    u32x4 kr[kBatch];
+    u32x4 kr[kBatch], vr[kBatch];
 #pragma unroll
-    for (int i = 0; i < kBatch; ++i) kr[i] = k_new[src0 + min(c0 + i * kThreads, nk - 1)];
+    for (int i = 0; i < kBatch; ++i) {
+      const int64_t c = src0 + min(c0 + i * kThreads, nk - 1);
+      kr[i] = k_new[c];
+      vr[i] = v_new[c];
+    }
 #pragma unroll
     for (int i = 0; i < kBatch; ++i) {
       const int c = c0 + i * kThreads;
       if (c < nk) {
         const int ch = c & (nch - 1);
         const int rest = c / nch;
-        kd[((rest % hkv) * kBs + rest / hkv) * nch + ch] = kr[i];
+        const int64_t o = dst0 + ((rest % hkv) * kBs + rest / hkv) * nch + ch;
+        k_cache[o] = kr[i];
+        v_cache[o] = vr[i];
       }
     }
-  }
-  if (v_active(tid)) v_store(tid);
-  for (int u = tid + kThreads; u < ntask; u += kThreads) {
-    if (!v_active(u)) continue;
-    v_load(u);
-    v_store(u);
   }
 }
 
@@ -184,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 // (8 wavefronts, two per SIMD) runs plan entries w, w + grid, w + 2 grid, ...
 // until an entry with r < 0, so one workgroup per CU walks its whole queue.
 //
-// Staging. LDS holds a ring of four stages of one 64-key step each (K and V^T
+// Staging. LDS holds a ring of four stages of one 64-key step each (K and V
 // of 4 blocks). A copy cursor, independent of the entry being computed, walks
 // the workgroup's queue three steps ahead of the computation and copies each
 // step's blocks into ring position p % 4 with load-to-LDS instructions (no
@@ -205,8 +166,9 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 // v_mfma_f32_32x32x16_bf16: in the 32x32 accumulator a lane then holds one
 // query column and 16 keys, so the softmax state is lane-local and a row
 // reduction needs one exchange with lane ^ 32 (v_permlane32_swap). O^T = V^T
-// P^T uses the packed probabilities as the B operand; the cache keeps each V
-// block transposed, so V operands are plain 16-byte reads.
+// P^T uses the packed probabilities as the B operand; its A operand (8
+// consecutive keys of one d per lane) comes from V rows staged token-major by
+// two transposing LDS reads (ds_read_b64_tr_b16).
 //
 // Softmax in base 2 with lazy rescaling. Q is pre-multiplied by
 // softmax_scale * log2(e) (rounded to bf16), and each S accumulator starts
@@ -221,16 +183,16 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(
 //  * K stages: each block of 16 keys chunk-major, [16-byte chunk c][key r]
 //    at c 256 + r 16: the 16 keys a read phase takes sit on distinct banks,
 //    and a lane's operand reads differ only by immediate offsets.
-//  * V stages (after the four K stages): each block as in the cache,
-//    [block][d][16 keys], 32-byte rows with the two 16-byte halves of row d
-//    swapped when bit 3 of d is set (conflict-free operand reads).
+//  * V stages (after the four K stages): chunk-major like K, key r of chunk c
+//    at slot r ^ 4 (c % 4): a transposing read takes 4 keys of 4 consecutive
+//    chunks, which this swizzle puts on distinct banks.
 //  * Key order: the PV MFMA's B operand is the score accumulator itself. In
 //    the 32x32 accumulator, lane half u, register e holds row
 //    8 (e / 4) + 4 u + e % 4. Reading K row pi(i) into A row i, with pi
 //    swapping bits 2 and 3 of i, makes that register hold key
 //    16 (e / 8) + 8 u + e % 8 (plus 32 per 32-key half), so for the 16-key
 //    slice kk of the PV product lane half u holds keys 16 kk + 8 u .. + 7 in
-//    order: block kk, half u of a V^T row, one 16-byte read.
+//    order: block kk, keys 8 u .. + 7 of one d, two transposing reads.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef const __attribute__((address_space(4))) int32_t cint32_t;
@@ -310,7 +272,7 @@ template <int D>
 struct AttnGeom {
   static constexpr int RB = 2 * D;              // bytes per K row
   static constexpr int KTILE = kKv * RB;        // K of one step
-  static constexpr int BLK = D * 2 * kBs;       // one V^T block (D rows of 16 keys)
+  static constexpr int BLK = kBs * RB;          // one V block (16 keys of D values)
   static constexpr int VTILE = (kKv / kBs) * BLK;
   static constexpr int KREG = kStages * KTILE;  // the V stages start here
   static constexpr int RING = KREG + kStages * VTILE;
@@ -405,17 +367,14 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   const uint32_t blk_bytes = uint32_t(a.hkv) * (kBs * RB);
   // Per-lane source offset inside a block and LDS destination of copy i
   // (relative to the wave's block slot in a stage; lane l lands at +16 l).
+  // Both tensors are staged chunk-major: 16-byte chunk c of key row r of a
+  // block at c 256 + r' 16, with r' = r for K and r' = r ^ 4 (c % 4) for V, so
+  // copy i (chunks 4 i .. 4 i + 3) brings lane l the chunk 4 i + l / 16 of key
+  // ckey (below).
+  const int ckey = is_v ? ((lane & 15) ^ ((lane >> 4) << 2)) : (lane & 15);
   uint32_t src_off[LPW];
 #pragma unroll
-  for (int i = 0; i < LPW; ++i) {
-    if (is_v) {
-      const int d = 32 * i + (lane >> 1);
-      src_off[i] = d * 32 + (((lane & 1) ^ ((lane >> 4) & 1)) << 4);
-    } else {
-      // K blocks are staged chunk-major: 16-byte chunk c of row r at c 256 + r 16
-      src_off[i] = (lane & 15) * RB + ((4 * i + (lane >> 4)) << 4);
-    }
-  }
+  for (int i = 0; i < LPW; ++i) src_off[i] = ckey * RB + ((4 * i + (lane >> 4)) << 4);
   // LDS address of this wave's block slot in ring position 0
   const uint32_t slot0 = lds0 + (is_v ? KREG + bs * BLK : bs * kBs * RB);
   const uint32_t stage_stride = is_v ? VTILE : KTILE;
@@ -563,16 +522,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       // (a missing block loads block 0 and discards it, so that every path
       // through here waits for the memory operations issued before it)
       u32x4 v = load16_now(src + src_off[i]);
-      if (is_v) {
-        // keys key0 + 8 h .. + 7 of row d, h the logical half this lane holds
-        const int h8 = 8 * ((lane & 1) ^ ((lane >> 4) & 1));
-        const int vn = b < 0 ? 0 : min(8, max(0, L - key0 - h8));
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = 2 * j + 1 < vn ? v[j] : (2 * j < vn ? (v[j] & 0xFFFFu) : 0u);
-      } else {
-        const bool ok = b >= 0 && key0 + (lane & 15) < L;
-        v = ok ? v : zero;
-      }
+      const bool ok = b >= 0 && key0 + ckey < L;
+      v = ok ? v : zero;
       *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
     }
     return false;
@@ -596,15 +547,30 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // plus h 32 RB + s 512.
   const int k_row = (l32 & ~12) | ((l32 & 4) << 1) | ((l32 & 8) >> 1);
   int k_off = (l32 >> 4) * (kBs * RB) + half * 256 + (k_row & 15) * 16;
-  // V operand: block kk, row d = 32 t + l32, logical half = half.
-  int v_off = KREG + l32 * 32 + ((half ^ ((l32 >> 3) & 1)) << 4);
+  // V operand (transposing reads, two per operand): in each 16-lane group a
+  // lane names 4 values of d of one key, and lane 4 q + s receives value s of
+  // the 4 keys named by lanes q, q + 4, q + 8, q + 12. Lane j of group gq names
+  // key 8 half + 4 rd + j / 4 of the block (rd: first or second read) and
+  // d = 32 t + 16 (gq % 2) + 4 (j % 4), so lane l32 receives row d = 32 t + l32,
+  // keys 8 half + 4 rd .. + 3: with both reads the operand of keys
+  // 8 half .. + 7. In the swizzled chunk-major layout that is the lane's base
+  // (chunk c % 4 = 2 (gq % 2) + (j % 4) / 2) plus t 1024 + kk BLK.
+  const int vj = lane & 15, vpart = 2 * ((lane >> 4) & 1) + ((vj & 3) >> 1);
+  int v_off0 = KREG + vpart * 256 + (((8 * half + (vj >> 2)) ^ (4 * vpart)) << 4) + 8 * (vj & 1);
+  int v_off1 = KREG + vpart * 256 + (((8 * half + 4 + (vj >> 2)) ^ (4 * vpart)) << 4) + 8 * (vj & 1);
   // Hide the bases' known bits from the compiler: otherwise it rewrites
   // base + constant as base | constant, which it cannot fold into the LDS
   // instructions' offset field, and keeps one register per read instead.
   asm volatile("" : "+v"(k_off));
-  asm volatile("" : "+v"(v_off));
+  asm volatile("" : "+v"(v_off0));
+  asm volatile("" : "+v"(v_off1));
   auto rd16 = [&](int addr) __attribute__((always_inline)) -> bf16x8 {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(lds + addr));
+  };
+  auto rdtr = [&](int addr) __attribute__((always_inline)) -> u32x2 {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    auto* lp = (__attribute__((address_space(3))) uint8_t*)lds + addr;
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)lp));
   };
 
   // This lane's query column inside a tile: head hh of the group, position pos.
@@ -767,7 +733,9 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       return rd16(kb + (i & 1) * 32 * RB + (i >> 1) * 512);
     };
     auto rdv = [&](int vb, int i) __attribute__((always_inline)) -> bf16x8 {
-      return rd16(vb + (i / DT) * BLK + (i % DT) * 1024);
+      const int o = vb + (i / DT) * BLK + (i % DT) * 1024;
+      const u32x2 lo = rdtr(v_off0 + o), hi = rdtr(v_off1 + o);
+      return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
     };
     // S^T = K Q^T of a step (no other work), accumulators from zero.
     auto qk_alone = [&](int kb, f32x16 (&sc)[2]) __attribute__((always_inline)) {
@@ -937,7 +905,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       }
     };
     auto kbase = [&](int pp) { return k_off + (pp & (kStages - 1)) * KTILE; };
-    auto vbase = [&](int pp) { return v_off + (pp & (kStages - 1)) * VTILE; };
+    auto vbase = [&](int pp) { return (pp & (kStages - 1)) * VTILE; };
 
     // ---- S(0) with the exact row maximum as base
     f32x16 sa[2], sb[2];
@@ -1154,7 +1122,7 @@ extern "C" cw_status cw_kv_append(const void* k_new, const void* v_new, void* k_
   hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(units)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(k_new),
                      static_cast<const u32x4*>(v_new), static_cast<u32x4*>(k_cache),
-                     static_cast<uint16_t*>(v_cache), block_table, bt_stride, cu_suffix_dev,
+                     static_cast<u32x4*>(v_cache), block_table, bt_stride, cu_suffix_dev,
                      prefix_len_dev, batch, num_kv_heads, head_dim, num_blocks);
   return check_launch("kv_append launch");
 }

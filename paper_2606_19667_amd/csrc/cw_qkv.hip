@@ -10,7 +10,7 @@
 //   y = x W^T (+ b)          x [T, hidden], W [(Hq + 2 Hkv) D, hidden]
 //   q, k = rope(y_q, y_k)    rotate-half form at position P_r + i
 //   q -> q_out [T, Hq, D];  k -> K cache [blk][g][slot][d];
-//   v -> V cache [blk][g][d][slot] (each block stored transposed)
+//   v -> V cache [blk][g][slot][d]
 //
 // Design (one workgroup = 8 wavefronts = one 256-feature x 256-token tile):
 //  * The product is formed as C^T = W x^T with v_mfma_f32_16x16x32_bf16:
@@ -249,17 +249,11 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
         uint16_t* qp = q_out + (int64_t(t) * hq + hf) * D + j;
         *reinterpret_cast<u32x2*>(qp) = u32x2{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3])};
         *reinterpret_cast<u32x2*>(qp + D / 2) = u32x2{pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
-      } else if (kind == 1) {
-        uint16_t* kp = k_cache + ((int64_t(blk) * hkv + g) * kBs + slot) * D + j;
-        *reinterpret_cast<u32x2*>(kp) = u32x2{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3])};
-        *reinterpret_cast<u32x2*>(kp + D / 2) = u32x2{pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
       } else {
-        uint16_t* vp = v_cache + ((int64_t(blk) * hkv + g) * D + j) * kBs + slot;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          vp[e * kBs] = uint16_t(pack_bf16x2(o0[e], 0.f));
-          vp[(e + D / 2) * kBs] = uint16_t(pack_bf16x2(o1[e], 0.f));
-        }
+        // k or v: row `slot` of the (block, head) in its cache, [blk][g][slot][d]
+        uint16_t* cp = (kind == 1 ? k_cache : v_cache) + ((int64_t(blk) * hkv + g) * kBs + slot) * D + j;
+        *reinterpret_cast<u32x2*>(cp) = u32x2{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3])};
+        *reinterpret_cast<u32x2*>(cp + D / 2) = u32x2{pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
       }
     }
   }

@@ -436,9 +436,9 @@ class BatchMeta:
 
 
 def _cache_shapes_ok(k_cache: torch.Tensor, v_cache: torch.Tensor, hkv: int, D: int) -> bool:
-    """K blocks are [slot][d], V blocks [d][slot]; both caches hold the same blocks."""
+    """Both caches are [num_blocks, Hkv, 16, D] (block rows are tokens)."""
     return (k_cache.dim() == 4 and v_cache.dim() == 4 and tuple(k_cache.shape[1:]) == (hkv, BLOCK_SIZE, D)
-            and tuple(v_cache.shape) == (k_cache.shape[0], hkv, D, BLOCK_SIZE))
+            and tuple(v_cache.shape) == tuple(k_cache.shape))
 
 
 def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor,
@@ -451,7 +451,7 @@ def kv_append(meta: BatchMeta, k_new: torch.Tensor, v_new: torch.Tensor, k_cache
         if tuple(t.shape) != (meta.total_rows, hkv, D):
             raise ValueError(f"{name} must be [{meta.total_rows}, {hkv}, {D}], got {tuple(t.shape)}")
     if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
-        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
     _check(_lib.cw_kv_append(_dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
                              _dev(k_cache, torch.bfloat16, "k_cache"), _dev(v_cache, torch.bfloat16, "v_cache"),
                              _dev(meta.bt, torch.int32, "block_table"), meta.bt_stride,
@@ -481,7 +481,7 @@ def qkv_rope_append(meta: BatchMeta, x: torch.Tensor, w: torch.Tensor, rope: tor
     if rope.dim() != 3 or tuple(rope.shape[1:]) != (D // 2, 2):
         raise ValueError(f"rope must be [n, {D // 2}, 2], got {tuple(rope.shape)}")
     if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
-        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
     if q_out is None:
         q_out = torch.empty((meta.total_rows, hq, D), dtype=torch.bfloat16, device=x.device)
     elif tuple(q_out.shape) != (meta.total_rows, hq, D):
@@ -507,7 +507,7 @@ def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
     if tuple(q.shape) != (meta.total_rows, hq, D):
         raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
     if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
-        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
     if out is None:
         out = torch.empty_like(q)
     elif tuple(out.shape) != tuple(q.shape):
@@ -549,7 +549,7 @@ def suffix_prefill_attn_split(meta: BatchMeta, q: torch.Tensor, k_cache: torch.T
     if tuple(q.shape) != (meta.total_rows, hq, D):
         raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
     if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
-        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
     if out is None:
         out = torch.empty_like(q)
     elif tuple(out.shape) != tuple(q.shape):
@@ -588,7 +588,7 @@ def suffix_prefill_attn_split_noalloc(meta: BatchMeta, q: torch.Tensor, k_cache:
     if tuple(q.shape) != (meta.total_rows, hq, D):
         raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
     if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
-        raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
     if out is None:
         out = torch.empty_like(q)
     elif tuple(out.shape) != tuple(q.shape):
@@ -725,7 +725,7 @@ class BatchRunner:
                             ("v_cache", v_cache, torch.bfloat16), ("out", out, torch.bfloat16)):
             _dev(t, dt, name)
         if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
-            raise ValueError("k_cache must be [num_blocks, Hkv, 16, D] and v_cache [num_blocks, Hkv, D, 16]")
+            raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
         self._tensors = (q, k_new, v_new, k_cache, v_cache, out)
         s = _stream(stream)
         p = self._p

@@ -101,7 +101,7 @@ def _append_check(w):
     expect_k = OP.kv_append_image(kb, _bits(db.k_new), db.sched.block_table, db.sched.cu_suffix,
                                   db.sched.prefix_len, w.block_size)
     expect_v = OP.kv_append_image(vb, _bits(db.v_new), db.sched.block_table, db.sched.cu_suffix,
-                                  db.sched.prefix_len, w.block_size, layout="d_slot")
+                                  db.sched.prefix_len, w.block_size)
     cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
     torch.cuda.synchronize()
     assert np.array_equal(_bits(db.k_cache), expect_k)
@@ -336,7 +336,7 @@ def test_kv_append_drops_out_of_pool_writes_bit_exact():
     expect_k = OP.kv_append_image(kb, _bits(db.k_new), db.sched.block_table, db.sched.cu_suffix,
                                   db.sched.prefix_len, w.block_size)
     expect_v = OP.kv_append_image(vb, _bits(db.v_new), db.sched.block_table, db.sched.cu_suffix,
-                                  db.sched.prefix_len, w.block_size, layout="d_slot")
+                                  db.sched.prefix_len, w.block_size)
     cw.kv_append(db.meta, db.k_new, db.v_new, db.k_cache, db.v_cache)
     torch.cuda.synchronize()
     assert np.array_equal(_bits(db.k_cache), expect_k)

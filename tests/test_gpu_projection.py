@@ -83,7 +83,7 @@ class Case:
         self.w = inputs.scaled_normal_bf16((seed, 102), (nf, hidden), hidden ** -0.5)
         self.b = inputs.scaled_normal_bf16((seed, 103), (nf,), 0.5) if bias else None
         self.k0 = inputs.normal_bf16((seed, 104), (num_blocks, hkv, BS, D))
-        self.v0 = inputs.normal_bf16((seed, 105), (num_blocks, hkv, D, BS))
+        self.v0 = inputs.normal_bf16((seed, 105), (num_blocks, hkv, BS, D))
         self.pos = PR.suffix_positions(self.cu, self.plen)
 
     def run(self):
@@ -108,7 +108,7 @@ class Case:
         T = int(self.cu[-1])
         ones = np.ones((T, self.hkv, self.D), bool)
         mk = _image(np.zeros(self.k0.shape, bool), ones, self.bt, self.cu, self.plen, "slot_d")
-        mv = _image(np.zeros(self.v0.shape, bool), ones, self.bt, self.cu, self.plen, "d_slot")
+        mv = _image(np.zeros(self.v0.shape, bool), ones, self.bt, self.cu, self.plen, "slot_d")
         return mk, mv
 
     def check_untouched(self):
@@ -123,7 +123,7 @@ class Case:
         _close(_f64(self.q), q, self.name + " q")
         mk, mv = self.check_untouched()
         ek = _image(_f64(self.k0), k, self.bt, self.cu, self.plen, "slot_d")
-        ev = _image(_f64(self.v0), v, self.bt, self.cu, self.plen, "d_slot")
+        ev = _image(_f64(self.v0), v, self.bt, self.cu, self.plen, "slot_d")
         _close(_f64(self.kc)[mk], ek[mk], self.name + " k cache")
         _close(_f64(self.vc)[mv], ev[mv], self.name + " v cache")
 
@@ -148,7 +148,7 @@ class Case:
             blk = int(self.bt[r, p // BS])
             if 0 <= blk < kc.shape[0]:
                 gk.append(kc[blk, :, p % BS, :])
-                gv.append(vc[blk, :, :, p % BS])
+                gv.append(vc[blk, :, p % BS, :])
                 ek.append(k[i])
                 ev.append(v[i])
         _close(np.stack(gk), np.stack(ek), self.name + " k cache (sampled rows)")

@@ -23,7 +23,7 @@ def test_exports_every_declared_symbol():
     lib = ctypes.CDLL(cw.LIB_PATH)
     for name in declared:
         assert hasattr(lib, name), name
-    assert cw.abi_version() == 3
+    assert cw.abi_version() == 4
 
 
 @pytest.mark.parametrize("n", [0, 1, 15, 16, 17, 100, 1408])
