@@ -12,13 +12,16 @@ warm-up queries were served.
 
 One step is one pass of the whole path over that batch:
   host   clone the pool state, cw_schedule_batch (chained hashes, prefix match,
-         allocation, commit), cw_suffix_prefill_plan, async copy of the block
-         table / offsets / plan through pinned buffers;
-  device cw_kv_append, then cw_suffix_prefill_attn (one attention layer);
+         allocation, commit), cw_suffix_prefill_append_plan, async copy of the
+         block table / offsets / plan through pinned buffers;
+  device cw_suffix_prefill_append_attn: the KV append and the attention of one
+         layer in one launch (the same cache image and output as cw_kv_append
+         followed by cw_suffix_prefill_attn);
   host   cw_release_batch.
 Inputs (Q and the new K/V rows, the cached prefix blocks) are resident in HBM
 before timing starts. K steps are timed between two device synchronisations;
-the attention kernel is also timed on its own with HIP events on its stream.
+the kernel is also timed on its own with HIP events on its stream. The same
+steps with the two separate calls are timed too (key separate_calls).
 
 Prints one JSON line. `value` is attention TFLOP/s over the whole step
 (algorithmic FLOPs 4 * D * Hq * sum_r (S_r P_r + S_r (S_r + 1) / 2)).
@@ -466,14 +469,19 @@ def main() -> int:
     # kernels wait for the upload (ev_up), and the host reuses r's pinned
     # buffer only once that upload has completed.
     copy_stream = torch.cuda.Stream(device=dev)
-    runners = []
-    for _ in range(2):
-        rn = cw.BatchRunner([p.tokens(w.seed) for p in w.prompts], stride, hq, hkv, D, w.block_size, device=dev)
-        rn.bind(db.q, db.k_new, db.v_new, db.k_cache, db.v_cache, out, w.scale, stream=stream)
-        rn.ev_up = None
-        rn.ev_done = None
-        runners.append(rn)
-    def step(i: int, ev=None):
+
+    def make_runners(fused: bool):
+        rs = []
+        for _ in range(2):
+            rn = cw.BatchRunner([p.tokens(w.seed) for p in w.prompts], stride, hq, hkv, D, w.block_size,
+                                device=dev, fused=fused)
+            rn.bind(db.q, db.k_new, db.v_new, db.k_cache, db.v_cache, out, w.scale, stream=stream)
+            rn.ev_up = None
+            rn.ev_done = None
+            rs.append(rn)
+        return rs
+
+    def step(runners, i: int, ev=None):
         rn = runners[i % 2]
         if rn.ev_up is not None:
             rn.ev_up.synchronize()
@@ -490,7 +498,13 @@ def main() -> int:
             rn.ev_up = torch.cuda.Event()
             rn.ev_up.record(copy_stream)
         stream.wait_event(rn.ev_up)
-        if ev is None:
+        if rn.fused:
+            if ev is not None:
+                ev[0].record(stream)
+            rn.append_attention()
+            if ev is not None:
+                ev[1].record(stream)
+        elif ev is None:
             rn.kv_append()
             rn.attention()
         else:
@@ -505,39 +519,46 @@ def main() -> int:
             rn.release(pool)
             pool.close()
 
-    step(0)
-    torch.cuda.synchronize()
-    if runners[0].total_rows != total_s or not np.array_equal(runners[0].plen_host, P):
-        raise RuntimeError("the scheduled batch differs from the prepared one")
+    def timed_steps(runners, warmup: int, settle_s: float):
+        """Settle and warm-up steps, then args.steps timed steps (wall clock),
+        then args.steps steps with HIP events around their kernels."""
+        step(runners, 0)
+        torch.cuda.synchronize()
+        if runners[0].total_rows != total_s or not np.array_equal(runners[0].plen_host, P):
+            raise RuntimeError("the scheduled batch differs from the prepared one")
+        n_settle = 0
+        t_settle = time.perf_counter()
+        while time.perf_counter() - t_settle < settle_s:
+            step(runners, n_settle)
+            n_settle += 1
+        for i in range(warmup):
+            step(runners, i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(runners, i)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            step(runners, args.steps + i, evs[i])
+        torch.cuda.synchronize()
+        return n_settle, ms, evs
+
+    # The step: the fused append + attention call (cw_suffix_prefill_append_attn).
     # Settle: the card's clocks take tens of milliseconds of sustained load to
     # reach their steady state (the attention kernel runs ~20 % slower in the
     # first few milliseconds), so untimed steps run for at least SETTLE_S
     # seconds before the warm-up steps, whatever --warmup is.
-    settle = 0
-    t_settle = time.perf_counter()
-    while time.perf_counter() - t_settle < SETTLE_S:
-        step(settle)
-        settle += 1
-    torch.cuda.synchronize()
-    print(f"[bench] settle {settle} steps, warmup {args.warmup} steps", file=sys.stderr, flush=True)
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(i)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed * 1e3 / args.steps
-    # Per-kernel durations: the same K steps again, with HIP events on the
-    # launch stream around each step's kv_append and attention launches (the
-    # event records cost step time, so the wall-clock pass above has none).
-    print(f"[bench] timing {args.steps} steps with per-kernel events", file=sys.stderr, flush=True)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    for i in range(args.steps):
-        step(args.steps + i, evs[i])
-    torch.cuda.synchronize()
+    print(f"[bench] timing {args.steps} fused steps", file=sys.stderr, flush=True)
+    fused_runners = make_runners(True)
+    settle, ms_per_step, evs = timed_steps(fused_runners, args.warmup, SETTLE_S)
+    fused_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    # The same steps with the two separate calls (cw_kv_append, then
+    # cw_suffix_prefill_attn), for the per-kernel breakdown.
+    print(f"[bench] timing {args.steps} steps of the separate calls", file=sys.stderr, flush=True)
+    runners = make_runners(False)
+    _, seq_ms_per_step, evs = timed_steps(runners, args.warmup, SETTLE_S)
     app_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
     attn_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
 
@@ -546,12 +567,13 @@ def main() -> int:
     # Per-call durations (hot caches) and with a 512 MB scratch buffer written
     # between calls, which evicts the K/V from L2 and the 256 MB MALL.
     hot = percentiles_us(timed_calls(rn.attention, stream, 50))
+    fused_hot = percentiles_us(timed_calls(fused_runners[(2 * args.steps - 1) % 2].append_attention, stream, 50))
     scratch = torch.empty(256 << 20, dtype=torch.bfloat16, device=dev)
     cold = percentiles_us(timed_calls(rn.attention, stream, 20, between=lambda: scratch.fill_(1.0)))
     del scratch
     host = host_timing(w, snapshot, stride) if trace_mode else None
 
-    achieved = flops / (attn_ms * 1e-3) / 1e12
+    achieved = flops / (fused_ms * 1e-3) / 1e12
     mfma_flops = executed_mfma_flops(sched.cu_suffix, P, hq, hkv, D)
     res = {
         "metric": "suffix-prefill attention TFLOP/s (whole step: schedule + kv_append + attention)",
@@ -573,23 +595,27 @@ def main() -> int:
                    "prefix_len": [int(x) for x in P]},
         "suffix_tokens_per_s": round(total_s / (ms_per_step * 1e-3), 1),
         "pct_bf16_peak_step": round(100 * flops / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
-        "attention_us": round(attn_ms * 1e3, 2),
-        "kv_append_us": round(app_ms * 1e3, 2),
-        "kv_append_GBps": round(append_bytes(S, hkv, D) / (app_ms * 1e-3) / 1e9, 1),
+        "step": "cw_suffix_prefill_append_attn (append and attention in one launch)",
+        "append_attention_us": round(fused_ms * 1e3, 2),
+        "separate_calls": {"ms_per_step": round(seq_ms_per_step, 5), "attention_us": round(attn_ms * 1e3, 2),
+                           "kv_append_us": round(app_ms * 1e3, 2),
+                           "kv_append_GBps": round(append_bytes(S, hkv, D) / (app_ms * 1e-3) / 1e9, 1),
+                           "attention_TFLOPs": round(flops / (attn_ms * 1e-3) / 1e12, 3)},
         "attention_GFLOP": round(flops / 1e9, 3),
         "attention_mfma_GFLOP": round(mfma_flops / 1e9, 3),
         "mfma_waste_factor": round(mfma_flops / flops, 4),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": counted_traffic(args.workload),
-                     "kernel": "suffix_prefill_attn_kernel<128, false>",
-                     "algorithmic_bytes": int(attention_bytes(P, S, hq, hkv, D))},
+                     "kernel": "suffix_prefill_attn_kernel<128, false, true>",
+                     "algorithmic_bytes": int(attention_bytes(P, S, hq, hkv, D)) + append_bytes(S, hkv, D) // 2},
         "attention_call_us": hot,
+        "append_attention_call_us": fused_hot,
         "attention_cold_us": cold,
     }
     if host is not None:
         res["host"] = host
-    del db, runners, out
+    del db, runners, fused_runners, out
     torch.cuda.empty_cache()
     if args.workload == "llama8b-trace-b16" and not args.no_diagnostic:
         print("[bench] question-only diagnostic point", file=sys.stderr, flush=True)

@@ -319,6 +319,65 @@ cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, const void*
                                  void* out, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Host: plan for cw_suffix_prefill_append_attn, the KV append and the
+ * attention of a batch in one call (paper Sec. 2.1: the suffix K/V go into
+ * their blocks; Sec. 1 and 2.1: the suffix rows attend over the cached prefix
+ * and themselves).
+ *
+ * The plan is the unsplit plan of cw_suffix_prefill_plan followed by a table
+ * with two words per (request, logical block): where the block's keys are read
+ * from and where the call writes them. A request's own suffix blocks are read
+ * from its rows of k_new / v_new and written to their cache blocks; a prefix
+ * block that is a full suffix block of this batch (a block an earlier request
+ * of the same schedule committed, R9) is read from those rows too; every
+ * other block is read from the caches. So the call reads no cache block it
+ * writes, and its result and cache image equal those of cw_kv_append followed
+ * by cw_suffix_prefill_attn. The header also fingerprints the block table and
+ * num_blocks: a plan is refused by a call whose host block table differs.
+ *   block_table_host  host int32 [batch, bt_stride], the table the caches use
+ *   plan_host         host int32 [plan_words]; copy all of it to device memory
+ * cw_suffix_prefill_append_plan_words returns the words (or a negative
+ * cw_status).
+ * CW_EINVAL: as cw_suffix_prefill_plan, plus a NULL table, num_blocks < 1,
+ *   ceil(L_r / 16) > bt_stride, P_r % 16 != 0, or an in-pool block named by
+ *   two suffix blocks of the batch (their appends would race).
+ * CW_EUNSUPPORTED: as cw_suffix_prefill_plan, plus a prefix block that is the
+ *   partial last block of a suffix of the batch (its bytes would be partly
+ *   appended rows and partly older content). */
+int64_t cw_suffix_prefill_append_plan_words(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                            int32_t bt_stride, int32_t batch, int32_t num_q_heads,
+                                            int32_t num_kv_heads, int32_t head_dim);
+cw_status cw_suffix_prefill_append_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                        const int32_t* block_table_host, int32_t bt_stride, int32_t batch,
+                                        int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                        int32_t num_blocks, int32_t* plan_host, int64_t plan_words);
+
+/* ------------------------------------------------------------------------
+ * Device: cw_kv_append and cw_suffix_prefill_attn in one launch (paper
+ * Sec. 2.1 and Sec. 1; the same result and cache image as the two calls in
+ * sequence). The tile whose query rows are a run of suffix positions also
+ * writes those positions' K and V rows of its KV head into their cache blocks,
+ * from the copy it stages for its own attention; all of the batch's new keys
+ * are read from k_new / v_new. Bytes of the caches outside the written rows
+ * are unchanged; writes to blocks outside [0, num_blocks) are dropped and such
+ * blocks read as zeros, as in the two calls.
+ *   k_new, v_new       bf16 [total_s, Hkv, D] device
+ *   k_cache, v_cache   written at the suffix rows, read elsewhere
+ *   block_table_host, cu_suffix_host, prefix_len_host   host copies; the
+ *                      kernel reads the device plan only (no device table or
+ *                      offsets are needed)
+ *   plan_host / plan_dev   the plan of cw_suffix_prefill_append_plan
+ * Errors as cw_suffix_prefill_attn; CW_EINVAL also for a plan without an append
+ * table or built for another block table or pool size. */
+cw_status cw_suffix_prefill_append_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                                        void* v_cache, const int32_t* block_table_host, int32_t bt_stride,
+                                        const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                        int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                        int32_t head_dim, int32_t block_size, int32_t num_blocks,
+                                        float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev,
+                                        void* out, void* stream);
+
+/* ------------------------------------------------------------------------
  * Device: split-KV variant of cw_suffix_prefill_attn, for batches with few
  * tiles (short suffixes such as a question after a fully cached evidence
  * prefix: paper Sec. 1 and 3.3, the reuse the ordering aims for). Same result

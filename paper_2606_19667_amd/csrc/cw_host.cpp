@@ -12,6 +12,7 @@
 #include <cstring>
 #include <numeric>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "cw_internal.h"
@@ -776,16 +777,73 @@ uint64_t batch_fingerprint(const int32_t* cu, const int32_t* plen, int32_t batch
 }
 }  // namespace cw
 
+namespace {
+
+// Entries and queues of a plan, and the words of its header and entries.
+struct PlanLayout {
+  std::vector<Entry> ents;
+  Queues qs;
+  int64_t padded = 0;   // queue slots (grid x longest queue)
+  int64_t words = 0;    // header + entries
+};
+
+PlanLayout plan_layout(const int32_t* cu, const int32_t* plen, int32_t batch, int32_t hq, int32_t hkv,
+                       int32_t splits) {
+  PlanLayout pl;
+  pl.ents = plan_entries(cu, plen, batch, hq, hkv, splits);
+  pl.qs = plan_queues(pl.ents, batch, hkv);
+  pl.padded = int64_t(pl.qs.grid) * pl.qs.len;
+  pl.words = cw::kPlanHeaderWords + cw::kPlanEntryWords * pl.padded;
+  return pl;
+}
+
+// Writes the header and the entries (queue slot i of workgroup w at entry
+// index i * grid + w) of a plan with fingerprint fp.
+void write_plan(const PlanLayout& pl, const int32_t* cu, int32_t batch, int32_t hq, int32_t hkv, int32_t d,
+                int32_t splits, uint64_t fp, int32_t* plan_host) {
+  const uint32_t lo = uint32_t(fp), hi = uint32_t(fp >> 32);
+  const Queues& qs = pl.qs;
+  int64_t work = 0;
+  for (const Entry& e : pl.ents) work += e.cost;
+  std::fill(plan_host, plan_host + pl.words, 0);
+  int32_t* h = plan_host;
+  h[cw::kHdrMagic] = cw::kPlanMagic;
+  h[cw::kHdrEntries] = int32_t(pl.padded);
+  h[cw::kHdrFpLo] = int32_t(lo);
+  h[cw::kHdrFpHi] = int32_t(hi);
+  h[cw::kHdrGrid] = qs.grid;
+  h[cw::kHdrSplits] = splits;
+  h[cw::kHdrBatch] = batch;
+  h[cw::kHdrHq] = hq;
+  h[cw::kHdrHkv] = hkv;
+  h[cw::kHdrD] = d;
+  h[cw::kHdrRows] = cu[batch];
+  h[cw::kHdrQueueLen] = qs.len;
+  h[cw::kHdrWork] = int32_t(std::min<int64_t>(work, INT32_MAX));
+  int32_t* body = plan_host + cw::kPlanHeaderWords;
+  for (int32_t w = 0; w < qs.grid; ++w)
+    for (int32_t i = 0; i < qs.len; ++i) {
+      int32_t* out = body + (int64_t(i) * qs.grid + w) * cw::kPlanEntryWords;
+      if (i < int32_t(qs.q[size_t(w)].size())) {
+        const Entry& e = pl.ents[size_t(qs.q[size_t(w)][size_t(i)])];
+        std::copy(e.f, e.f + cw::kEntFields, out);
+      } else {
+        out[cw::kEntR] = -1;   // end of this queue
+      }
+      out[cw::kEntCheck] = int32_t(cw::entry_tag(lo, hi, uint32_t(int64_t(i) * qs.grid + w)));
+    }
+}
+
+}  // namespace
+
 extern "C" int64_t cw_suffix_prefill_plan_words(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
                                                 int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                                 int32_t head_dim, int32_t num_splits) {
   cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim, num_splits);
   if (st != CW_OK) return st;
-  const std::vector<Entry> ents = plan_entries(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
-                                               num_splits);
-  const Queues qs = plan_queues(ents, batch, num_kv_heads);
+  const PlanLayout pl = plan_layout(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, num_splits);
   cw::ok();
-  return cw::kPlanHeaderWords + int64_t(cw::kPlanEntryWords) * qs.grid * qs.len;
+  return pl.words;
 }
 
 extern "C" cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
@@ -794,46 +852,144 @@ extern "C" cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const
                                             int64_t plan_words) {
   cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim, num_splits);
   if (st != CW_OK) return st;
-  const std::vector<Entry> ents = plan_entries(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
-                                               num_splits);
-  const Queues qs = plan_queues(ents, batch, num_kv_heads);
-  const int64_t padded = int64_t(qs.grid) * qs.len;
-  const int64_t need = cw::kPlanHeaderWords + cw::kPlanEntryWords * padded;
-  if (padded > INT32_MAX / cw::kPlanEntryWords) return fail(CW_EUNSUPPORTED, "too many plan entries");
-  if (!plan_host || plan_words < need)
-    return fail(CW_EINVAL, "plan buffer too small: need " + std::to_string(need) + " words");
+  const PlanLayout pl = plan_layout(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, num_splits);
+  if (pl.padded > INT32_MAX / cw::kPlanEntryWords) return fail(CW_EUNSUPPORTED, "too many plan entries");
+  if (!plan_host || plan_words < pl.words)
+    return fail(CW_EINVAL, "plan buffer too small: need " + std::to_string(pl.words) + " words");
   const uint64_t fp = cw::batch_fingerprint(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
                                             head_dim, num_splits);
-  const uint32_t lo = uint32_t(fp), hi = uint32_t(fp >> 32);
-  int64_t work = 0;
-  for (const Entry& e : ents) work += e.cost;
-  std::fill(plan_host, plan_host + need, 0);
-  int32_t* h = plan_host;
-  h[cw::kHdrMagic] = cw::kPlanMagic;
-  h[cw::kHdrEntries] = int32_t(padded);
-  h[cw::kHdrFpLo] = int32_t(lo);
-  h[cw::kHdrFpHi] = int32_t(hi);
-  h[cw::kHdrGrid] = qs.grid;
-  h[cw::kHdrSplits] = num_splits;
-  h[cw::kHdrBatch] = batch;
-  h[cw::kHdrHq] = num_q_heads;
-  h[cw::kHdrHkv] = num_kv_heads;
-  h[cw::kHdrD] = head_dim;
-  h[cw::kHdrRows] = cu_suffix_host[batch];
-  h[cw::kHdrQueueLen] = qs.len;
-  h[cw::kHdrWork] = int32_t(std::min<int64_t>(work, INT32_MAX));
-  int32_t* body = plan_host + cw::kPlanHeaderWords;
-  for (int32_t w = 0; w < qs.grid; ++w)
-    for (int32_t i = 0; i < qs.len; ++i) {
-      int32_t* out = body + (int64_t(i) * qs.grid + w) * cw::kPlanEntryWords;
-      if (i < int32_t(qs.q[size_t(w)].size())) {
-        const Entry& e = ents[size_t(qs.q[size_t(w)][size_t(i)])];
-        std::copy(e.f, e.f + cw::kEntFields, out);
-      } else {
-        out[cw::kEntR] = -1;   // end of this queue
-      }
-      out[cw::kEntCheck] = int32_t(cw::entry_tag(lo, hi, uint32_t(int64_t(i) * qs.grid + w)));
+  write_plan(pl, cu_suffix_host, batch, num_q_heads, num_kv_heads, head_dim, num_splits, fp, plan_host);
+  return cw::ok();
+}
+
+namespace cw {
+uint64_t append_fingerprint(const int32_t* cu, const int32_t* plen, const int32_t* bt, int32_t bt_stride,
+                            int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t num_blocks) {
+  uint64_t h = batch_fingerprint(cu, plen, batch, hq, hkv, d, 1) ^ 0x9E3779B97F4A7C15ULL;
+  auto add = [&](uint32_t w) {
+    for (int i = 0; i < 4; ++i) {
+      h ^= (w >> (8 * i)) & 0xFFu;
+      h *= 0x100000001b3ULL;
     }
+  };
+  add(uint32_t(num_blocks));
+  add(uint32_t(bt_stride));
+  for (int32_t r = 0; r < batch; ++r) {
+    const int64_t nb = (int64_t(plen[r]) + cu[r + 1] - cu[r] + kBlockSize - 1) / kBlockSize;
+    for (int64_t j = 0; j < nb; ++j) add(uint32_t(bt[int64_t(r) * bt_stride + j]));
+  }
+  h ^= h >> 33;
+  h *= 0xc4ceb9fe1a85ec53ULL;
+  h ^= h >> 33;
+  return h;
+}
+}  // namespace cw
+
+namespace {
+
+// Checks of the fused plan's arguments beyond plan_args (one split).
+cw_status append_plan_args(const int32_t* cu, const int32_t* plen, const int32_t* bt, int32_t bt_stride,
+                           int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t num_blocks) {
+  cw_status st = plan_args(cu, plen, batch, hq, hkv, d, 1);
+  if (st != CW_OK) return st;
+  if (!bt) return fail(CW_EINVAL, "block_table_host is required");
+  if (num_blocks < 1) return fail(CW_EINVAL, "num_blocks must be >= 1");
+  if (num_blocks > cw::kMaxAppendBlocks) return fail(CW_EUNSUPPORTED, "num_blocks must be below 2^27");
+  int64_t rows = 0;
+  return cw::check_batch(cu, plen, batch, cw::kBlockSize, bt_stride, &rows);
+}
+
+int64_t append_table_words(int32_t batch, int32_t bt_stride) { return int64_t(batch) * bt_stride * 2; }
+
+// The fused plan's table (layout in cw_internal.h). With cw_kv_append run
+// before the attention call, a request reads its own suffix blocks after the
+// append, and a prefix block that is some request's full suffix block of this
+// batch (a block committed earlier in the same schedule) also holds the rows
+// appended into it: both are read from those rows of k_new / v_new instead,
+// so that the fused call computes what the two calls in sequence compute
+// while nothing in it reads a block it writes. Refused: a suffix block named
+// twice (the two appends would race) and a prefix block that is a partial
+// suffix block (its bytes would be part appended rows, part older content).
+cw_status build_append_table(const int32_t* cu, const int32_t* plen, const int32_t* bt, int32_t bt_stride,
+                             int32_t batch, int32_t num_blocks, int32_t* table) {
+  constexpr int32_t bs = cw::kBlockSize;
+  std::unordered_map<int32_t, int32_t> fresh;   // suffix block -> first row (-1: partial block)
+  for (int32_t r = 0; r < batch; ++r) {
+    const int32_t P = plen[r], L = P + (cu[r + 1] - cu[r]);
+    for (int32_t j = P / bs; j < (L + bs - 1) / bs; ++j) {
+      const int32_t id = bt[int64_t(r) * bt_stride + j];
+      if (id < 0 || id >= num_blocks) continue;
+      const int32_t row = (j + 1) * bs <= L ? cu[r] + (j * bs - P) : -1;
+      if (!fresh.emplace(id, row).second)
+        return fail(CW_EINVAL, "block " + std::to_string(id) + " is named by two suffix blocks of the batch");
+    }
+  }
+  std::fill(table, table + append_table_words(batch, bt_stride), -1);
+  for (int32_t r = 0; r < batch; ++r) {
+    const int32_t P = plen[r], L = P + (cu[r + 1] - cu[r]);
+    for (int32_t j = 0; j < (L + bs - 1) / bs; ++j) {
+      const int32_t id = bt[int64_t(r) * bt_stride + j];
+      int32_t* t = table + (int64_t(r) * bt_stride + j) * 2;
+      const bool in_pool = id >= 0 && id < num_blocks;
+      if (j >= P / bs) {   // a suffix block of r: its rows, and the append target
+        if (in_pool) {
+          t[0] = cw::append_src_rows(cu[r] + (j * bs - P));
+          t[1] = id;
+        }
+        continue;
+      }
+      if (!in_pool) continue;   // no block: zeros
+      const auto it = fresh.find(id);
+      if (it == fresh.end()) {
+        t[0] = cw::append_src_block(id);
+      } else if (it->second >= 0) {
+        t[0] = cw::append_src_rows(it->second);
+      } else {
+        return fail(CW_EUNSUPPORTED, "a prefix block of request " + std::to_string(r) +
+                                         " is the partial last block of a suffix in the same batch");
+      }
+    }
+  }
+  return CW_OK;
+}
+
+}  // namespace
+
+extern "C" int64_t cw_suffix_prefill_append_plan_words(const int32_t* cu_suffix_host,
+                                                       const int32_t* prefix_len_host, int32_t bt_stride,
+                                                       int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                                       int32_t head_dim) {
+  cw_status st = plan_args(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim, 1);
+  if (st != CW_OK) return st;
+  if (bt_stride < 1) return fail(CW_EINVAL, "bt_stride must be >= 1");
+  const PlanLayout pl = plan_layout(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, 1);
+  cw::ok();
+  return pl.words + append_table_words(batch, bt_stride);
+}
+
+extern "C" cw_status cw_suffix_prefill_append_plan(const int32_t* cu_suffix_host, const int32_t* prefix_len_host,
+                                                   const int32_t* block_table_host, int32_t bt_stride,
+                                                   int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                                   int32_t head_dim, int32_t num_blocks, int32_t* plan_host,
+                                                   int64_t plan_words) {
+  cw_status st = append_plan_args(cu_suffix_host, prefix_len_host, block_table_host, bt_stride, batch, num_q_heads,
+                                  num_kv_heads, head_dim, num_blocks);
+  if (st != CW_OK) return st;
+  const PlanLayout pl = plan_layout(cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, 1);
+  if (pl.padded > INT32_MAX / cw::kPlanEntryWords) return fail(CW_EUNSUPPORTED, "too many plan entries");
+  const int64_t need = pl.words + append_table_words(batch, bt_stride);
+  if (need > INT32_MAX) return fail(CW_EUNSUPPORTED, "plan too large");
+  if (!plan_host || plan_words < need)
+    return fail(CW_EINVAL, "plan buffer too small: need " + std::to_string(need) + " words");
+  st = build_append_table(cu_suffix_host, prefix_len_host, block_table_host, bt_stride, batch, num_blocks,
+                          plan_host + pl.words);
+  if (st != CW_OK) return st;
+  const uint64_t fp = cw::append_fingerprint(cu_suffix_host, prefix_len_host, block_table_host, bt_stride, batch,
+                                             num_q_heads, num_kv_heads, head_dim, num_blocks);
+  write_plan(pl, cu_suffix_host, batch, num_q_heads, num_kv_heads, head_dim, 1, fp, plan_host);
+  plan_host[cw::kHdrTable] = int32_t(pl.words);
+  plan_host[cw::kHdrTableStride] = bt_stride;
+  plan_host[cw::kHdrNumBlocks] = num_blocks;
   return cw::ok();
 }
 
@@ -842,18 +998,28 @@ extern "C" cw_status cw_suffix_prefill_plan(const int32_t* cu_suffix_host, const
 namespace cw {
 cw_status check_plan_header(const char* what, const int32_t* plan_host, const int32_t* cu, const int32_t* plen,
                             int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t* grid, int32_t* splits,
-                            uint32_t* fp_lo, uint32_t* fp_hi, int32_t* num_entries) {
+                            uint32_t* fp_lo, uint32_t* fp_hi, int32_t* num_entries, const int32_t* append_bt,
+                            int32_t bt_stride, int32_t num_blocks) {
   const std::string w(what);
   if (!plan_host) return fail(CW_EINVAL, w + ": plan_host is required");
   if (plan_host[kHdrMagic] != kPlanMagic) return fail(CW_EINVAL, w + ": plan_host is not a plan of this library");
   const int32_t s = plan_host[kHdrSplits];
   if (s < 1 || s > kMaxSplits) return fail(CW_EINVAL, w + ": plan has an invalid split count");
-  const uint64_t fp = batch_fingerprint(cu, plen, batch, hq, hkv, d, s);
+  if (!append_bt && plan_host[kHdrTable] != 0)
+    return fail(CW_EINVAL, w + ": the plan carries an append table (cw_suffix_prefill_append_plan): "
+                               "use cw_suffix_prefill_append_attn");
+  if (append_bt && plan_host[kHdrTable] == 0)
+    return fail(CW_EINVAL, w + ": the plan has no append table: build it with cw_suffix_prefill_append_plan");
+  const uint64_t fp = append_bt ? append_fingerprint(cu, plen, append_bt, bt_stride, batch, hq, hkv, d, num_blocks)
+                                : batch_fingerprint(cu, plen, batch, hq, hkv, d, s);
   if (uint32_t(plan_host[kHdrFpLo]) != uint32_t(fp) || uint32_t(plan_host[kHdrFpHi]) != uint32_t(fp >> 32) ||
       plan_host[kHdrBatch] != batch || plan_host[kHdrHq] != hq || plan_host[kHdrHkv] != hkv || plan_host[kHdrD] != d)
     return fail(CW_EINVAL, w + ": the plan was built for another batch (cu_suffix, prefix_len, heads or head_dim differ)");
   const int32_t g = plan_host[kHdrGrid], len = plan_host[kHdrQueueLen], n = plan_host[kHdrEntries];
   if (g < 0 || g > kNumCu || len < 0 || int64_t(g) * len != n)
+    return fail(CW_EINVAL, w + ": plan header is inconsistent");
+  if (append_bt && (s != 1 || plan_host[kHdrTableStride] != bt_stride || plan_host[kHdrNumBlocks] != num_blocks ||
+                    int64_t(plan_host[kHdrTable]) != kPlanHeaderWords + int64_t(kPlanEntryWords) * n))
     return fail(CW_EINVAL, w + ": plan header is inconsistent");
   *grid = g;
   *splits = s;

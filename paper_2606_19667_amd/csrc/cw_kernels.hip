@@ -238,6 +238,15 @@ __device__ __forceinline__ int32_t load_word_untracked_s(const int32_t* base) {
   asm volatile("global_load_dword %0, %1, %2" : "=v"(v) : "v"(0u), "s"(bu));
   return v;
 }
+// Two words (8-byte aligned) at a wave-uniform address, completion untracked.
+__device__ __forceinline__ u32x2 load_pair_untracked_s(const int32_t* base) {
+  const uint64_t b = reinterpret_cast<uintptr_t>(base);
+  const uint64_t bu = (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b >> 32)))) << 32) |
+                      uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b))));
+  u32x2 v;
+  asm volatile("global_load_dwordx2 %0, %1, %2" : "=v"(v) : "v"(0u), "s"(bu));
+  return v;
+}
 
 // Brings the 128-byte line holding src (per lane) into L2 with a 4-byte
 // load-to-LDS per lane into lds_addr + 4 l, an area whose bytes nothing reads;
@@ -247,19 +256,21 @@ __device__ __forceinline__ void touch_line(const void* src, uint32_t lds_addr) {
                :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
 }
 
-// One load-to-LDS copy: lane l's 16 bytes at base + off land at lds + 16 l.
-// base is wave-uniform (SGPRs), off a per-lane 32-bit offset; M0 holds the LDS
-// address (one wait state between writing M0 and the copy).
+// One load-to-LDS copy: lane l's 16 bytes at base + off + 64 k land at
+// lds + 16 l (k = 0 .. 3). base is wave-uniform (SGPRs), off a per-lane 32-bit
+// offset; M0 holds the LDS address (one wait state between writing M0 and the
+// copy). The instruction's immediate offset is not used for the 64 k: it would
+// move the LDS destination as well.
 // (The uniform operands go through readfirstlane: the values are wave-uniform,
 // and this keeps them in SGPRs where the compiler cannot prove it.)
-__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t off, uint32_t lds_addr) {
+__device__ __forceinline__ void copy16_to_lds(const void* base, uint32_t off, uint32_t lds_addr, int k) {
   const uint64_t b = reinterpret_cast<uintptr_t>(base);
   // readfirstlane returns int: widen through uint32_t so the low half is not
   // sign-extended into the high half
   const uint64_t bu = (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b >> 32)))) << 32) |
                       uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(b))));
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(off), "s"(bu), "s"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
+               :: "v"(off + 64u * uint32_t(k)), "s"(bu), "s"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
 }
 
 constexpr int kAttnWaves = 8;
@@ -318,13 +329,18 @@ struct AttnArgs {
   const uint16_t* q;
   const uint16_t* kc;
   const uint16_t* vc;
-  const int32_t* bt;
+  const int32_t* bt;     // block table; for FUSED the plan's table of (source, destination) pairs
   const int32_t* plan;   // device copy of the whole plan (header, then entries)
+  const uint16_t* kn;    // FUSED: the suffix K / V rows [total_s, Hkv, D]
+  const uint16_t* vn;
+  uint16_t* kw;          // FUSED: the caches, written at the suffix blocks
+  uint16_t* vw;
   uint16_t* out;
   float* part_o;         // split runs: normalised O per run, fp32
   float* part_lse;       // split runs: base-2 log-sum-exp per run
   int64_t part_rows;     // rows of one run's part: total_s * Hq
   int32_t bt_stride, hq, hkv, group, per_tile, num_blocks, num_entries;
+  int32_t total_rows;    // FUSED: rows of k_new / v_new
   float c_log2;
   uint32_t fp_lo, fp_hi; // the batch fingerprint the host validated
 };
@@ -335,9 +351,17 @@ struct AttnArgs {
 // part_o[split][row][d] and the base-2 log-sum-exp of the scaled scores to
 // part_lse[split][row] (row = suffix row * Hq + head), -inf when no key of the
 // run is visible. lse_merge_kernel combines the runs.
-template <int D, bool SPLIT>
+//
+// FUSED (unsplit only): the KV append happens inside the call. The table of
+// the plan gives each logical block a source (a cache block, 16 rows of
+// k_new / v_new, or nothing) and a destination: a block whose rows are this
+// call's suffix rows is staged from k_new / v_new, and the entry whose query
+// rows are those rows also writes them, from the LDS stage, into the block's
+// place in the caches. No entry reads a cache block that the call writes.
+template <int D, bool SPLIT, bool FUSED>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void suffix_prefill_attn_kernel(const AttnArgs a) {
+  static_assert(!(SPLIT && FUSED), "the fused call is unsplit");
   using G = AttnGeom<D>;
   constexpr int KS = G::KS, DT = G::DT, RB = G::RB, LPW = G::LPW;
   constexpr int KTILE = G::KTILE, BLK = G::BLK, VTILE = G::VTILE, KREG = G::KREG;
@@ -371,10 +395,20 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // block at c 256 + r' 16, with r' = r for K and r' = r ^ 4 (c % 4) for V, so
   // copy i (chunks 4 i .. 4 i + 3) brings lane l the chunk 4 i + l / 16 of key
   // ckey (below).
+  // ckey (below). Copy i adds 64 i (its immediate offset) to the lane's base:
+  // off_c for a cache block (rows RB apart), off_n for rows of k_new / v_new
+  // (rows Hkv RB apart).
   const int ckey = is_v ? ((lane & 15) ^ ((lane >> 4) << 2)) : (lane & 15);
-  uint32_t src_off[LPW];
-#pragma unroll
-  for (int i = 0; i < LPW; ++i) src_off[i] = ckey * RB + ((4 * i + (lane >> 4)) << 4);
+  const uint32_t off_c = uint32_t(ckey * RB + ((lane >> 4) << 4));
+  const uint32_t row_bytes = uint32_t(a.hkv) * RB;   // FUSED: from one k_new row to the next
+  const uint32_t off_n = FUSED ? uint32_t(ckey) * row_bytes + uint32_t((lane >> 4) << 4) : 0u;
+  const uint8_t* const fresh_base = reinterpret_cast<const uint8_t*>(is_v ? a.vn : a.kn);
+  // FUSED: largest source index of a whole block: cache blocks (16 b) and
+  // k_new / v_new rows (the host refuses pools of 2^27 blocks or more)
+  const int cache_lim = 16 * a.num_blocks - 16;
+  const int fresh_lim = a.total_rows - 16;
+  // table words per logical block
+  constexpr int TW = FUSED ? 2 : 1;
   // LDS address of this wave's block slot in ring position 0
   const uint32_t slot0 = lds0 + (is_v ? KREG + bs * BLK : bs * kBs * RB);
   const uint32_t stage_stride = is_v ? VTILE : KTILE;
@@ -397,6 +431,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   const int32_t* c_row = a.bt;   // block-table row of the cursor's request
   const int32_t* c_ptr = a.bt;   // table word of this wave's block at the cursor's step
   const uint8_t* c_src = cache;  // this wave's tensor at the cursor's KV head
+  int64_t c_delta = 0;   // FUSED: from c_src to this wave's tensor at that head in k_new / v_new
   bool cdone = false;
   auto entry_word_addr = [&](int e) __attribute__((always_inline)) -> const int32_t* {
     return ents + int64_t(min(e, a.num_entries - 1)) * kEntryWords + (lane & 15);
@@ -417,9 +452,11 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     c_L = __builtin_amdgcn_readlane(cdesc, cw::kEntL);
     c_whole = c_L / kBs;
     c_last = (c_L + kBs - 1) / kBs - 1;
-    c_row = a.bt + int64_t(r) * a.bt_stride;
-    c_ptr = c_row + c_lb;
-    c_src = cache + int64_t(__builtin_amdgcn_readlane(cdesc, cw::kEntG)) * (kBs * RB);
+    c_row = a.bt + int64_t(r) * a.bt_stride * TW;
+    c_ptr = c_row + c_lb * TW;
+    const int cg = __builtin_amdgcn_readlane(cdesc, cw::kEntG);
+    c_src = cache + int64_t(cg) * (kBs * RB);
+    if constexpr (FUSED) c_delta = (fresh_base + int64_t(cg) * RB) - c_src;
     // Fast steps: not the entry's last (whose issue() enters the next entry),
     // the block whole (lb < c_whole) and the next step's table word inside
     // the prompt's blocks (lb + 4 <= c_last), so that it needs no clamp.
@@ -440,16 +477,23 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       } while (!cdone && c_left == 0);
     }
   };
-  // Block-table word of this wave's block at the cursor's step, loaded one
-  // step before its copies: issue() loads it before its own copies, so the
-  // step barrier that follows (which leaves only those copies in flight)
-  // completes it. The index is clamped into the prompt. Past the last entry a
-  // harmless word (the plan's first) is loaded.
-  int32_t bword = 0;
-  auto cursor_load = [&]() __attribute__((always_inline)) {
-    c_ptr = c_row + min(c_lb, c_last);
-    bword = load_word_untracked_s(cdone ? a.plan : c_ptr);
+  // Block-table word (FUSED: the table's pair) of this wave's block at the
+  // cursor's step, loaded one step before its copies: issue() loads it before
+  // its own copies, so the step barrier that follows (which leaves only those
+  // copies in flight) completes it. The index is clamped into the prompt. Past
+  // the last entry harmless words (the plan's first) are loaded.
+  std::conditional_t<FUSED, u32x2, int32_t> bword{};
+  auto load_bword = [&](const int32_t* w) __attribute__((always_inline)) {
+    if constexpr (FUSED) bword = load_pair_untracked_s(w);
+    else bword = load_word_untracked_s(w);
   };
+  auto cursor_load = [&]() __attribute__((always_inline)) {
+    c_ptr = c_row + min(c_lb, c_last) * TW;
+    load_bword(cdone ? a.plan : c_ptr);
+  };
+  // FUSED: the destination word of the block each ring position holds (lane
+  // p % 4), recorded when the block is copied, -1 when nothing is written.
+  int32_t dring = -1;
   cursor_enter();
   cursor_load();
   // The copies of a step are spread over the step's MFMAs rather than issued
@@ -458,9 +502,9 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // a step without load-to-LDS copies rewrites this wave's own area with bytes
   // of block 0, which nothing reads (the step then waits for all).
   uint64_t cp_src = reinterpret_cast<uintptr_t>(cache);
-  uint32_t cp_dst = own_area, cp_stride = 0;
+  uint32_t cp_dst = own_area, cp_stride = 0, cp_off = off_c;
   auto copy_part = [&](int k) __attribute__((always_inline)) {
-    copy16_to_lds(reinterpret_cast<const void*>(cp_src), src_off[k], cp_dst + k * cp_stride);
+    copy16_to_lds(reinterpret_cast<const void*>(cp_src), cp_off, cp_dst + k * cp_stride, k);
   };
   // Copies the cursor's step into ring position p (now, or through copy_part
   // when `spread`) and advances the cursor. Returns whether load-to-LDS
@@ -469,64 +513,156 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
   // completed by the wait before this call.
   auto issue = [&](int p, bool spread) __attribute__((always_inline)) -> bool {
     asm volatile("" : "+v"(bword));
-    const int raw = __builtin_amdgcn_readfirstlane(bword);
+    int raw, dword = -1;
+    if constexpr (FUSED) {
+      raw = __builtin_amdgcn_readfirstlane(int(bword[0]));
+      dword = __builtin_amdgcn_readfirstlane(int(bword[1]));
+    } else {
+      raw = __builtin_amdgcn_readfirstlane(bword);
+    }
     const uint32_t dst = slot0 + uint32_t(p & (kStages - 1)) * stage_stride;
-    // fast path: a whole block inside the pool, the next word inside the
-    // prompt's blocks, the cursor stays in its entry (c_fast > 0 implies
-    // !cdone)
-    if (c_fast > 0 && uint32_t(raw) < uint32_t(a.num_blocks)) {
-      const uint8_t* src = c_src + uint64_t(uint32_t(raw)) * blk_bytes;
-      --c_fast;
-      --c_left;
+    if constexpr (!FUSED) {
+      // fast path: a whole block inside the pool, the next word inside the
+      // prompt's blocks, the cursor stays in its entry (c_fast > 0 implies
+      // !cdone)
+      if (c_fast > 0 && uint32_t(raw) < uint32_t(a.num_blocks)) {
+        const uint8_t* src = c_src + uint64_t(uint32_t(raw)) * blk_bytes;
+        --c_fast;
+        --c_left;
+        c_lb += kKv / kBs;
+        c_ptr += kKv / kBs;
+        load_bword(c_ptr);
+        if (spread) {
+          cp_src = reinterpret_cast<uintptr_t>(src);
+          cp_dst = dst;
+          cp_stride = 1024;
+        } else {
+#pragma unroll
+          for (int i = 0; i < LPW; ++i) copy16_to_lds(src, off_c, dst + i * 1024, i);
+        }
+        return true;
+      }
+      cp_src = reinterpret_cast<uintptr_t>(cache);
+      cp_dst = own_area;
+      cp_stride = 0;
+      if (cdone) return false;
+      const int lb = c_lb, L = c_L;
+      // physical block, or -1 past the prompt / outside the pool
+      const int b = (lb <= c_last && uint32_t(raw) < uint32_t(a.num_blocks)) ? raw : -1;
+      const bool whole = b >= 0 && lb < c_whole;
+      const uint8_t* src = c_src + uint64_t(uint32_t(b < 0 ? 0 : b)) * blk_bytes;
       c_lb += kKv / kBs;
-      c_ptr += kKv / kBs;
-      bword = load_word_untracked_s(c_ptr);
-      if (spread) {
-        cp_src = reinterpret_cast<uintptr_t>(src);
-        cp_dst = dst;
-        cp_stride = 1024;
-      } else {
+      c_fast = max(0, c_fast - 1);
+      if (--c_left == 0) cursor_enter();
+      cursor_load();
+      if (whole) {   // wave-uniform: the whole block is valid
+        if (spread) {
+          cp_src = reinterpret_cast<uintptr_t>(src);
+          cp_dst = dst;
+          cp_stride = 1024;
+        } else {
 #pragma unroll
-        for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
+          for (int i = 0; i < LPW; ++i) copy16_to_lds(src, off_c, dst + i * 1024, i);
+        }
+        return true;
       }
-      return true;
-    }
-    cp_src = reinterpret_cast<uintptr_t>(cache);
-    cp_dst = own_area;
-    cp_stride = 0;
-    if (cdone) return false;
-    const int lb = c_lb, L = c_L;
-    // physical block, or -1 past the prompt / outside the pool
-    const int b = (lb <= c_last && uint32_t(raw) < uint32_t(a.num_blocks)) ? raw : -1;
-    const bool whole = b >= 0 && lb < c_whole;
-    const uint8_t* src = c_src + uint64_t(uint32_t(b < 0 ? 0 : b)) * blk_bytes;
-    c_lb += kKv / kBs;
-    c_fast = max(0, c_fast - 1);
-    if (--c_left == 0) cursor_enter();
-    cursor_load();
-    if (whole) {   // wave-uniform: the whole block is valid
-      if (spread) {
-        cp_src = reinterpret_cast<uintptr_t>(src);
-        cp_dst = dst;
-        cp_stride = 1024;
-      } else {
+      const int key0 = lb * kBs;
+      const u32x4 zero{0, 0, 0, 0};
 #pragma unroll
-        for (int i = 0; i < LPW; ++i) copy16_to_lds(src, src_off[i], dst + i * 1024);
+      for (int i = 0; i < LPW; ++i) {
+        // (a missing block loads block 0 and discards it, so that every path
+        // through here waits for the memory operations issued before it)
+        u32x4 v = load16_now(src + off_c + 64 * i);
+        const bool ok = b >= 0 && key0 + ckey < L;
+        v = ok ? v : zero;
+        *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
       }
-      return true;
-    }
-    const int key0 = lb * kBs;
-    const u32x4 zero{0, 0, 0, 0};
-#pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-      // (a missing block loads block 0 and discards it, so that every path
-      // through here waits for the memory operations issued before it)
-      u32x4 v = load16_now(src + src_off[i]);
-      const bool ok = b >= 0 && key0 + ckey < L;
-      v = ok ? v : zero;
-      *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
-    }
-    return false;
+      return false;
+    } else {
+      // The block's source: the cache block raw (FUSED: the word is 16 b for
+      // cache block b, or 0x80000000 | R for rows R .. R + 15 of k_new / v_new,
+      // both scaled by row_bytes; -1 or any other value out of range is no
+      // block). `inb`: a whole block of that source lies inside its tensor.
+      // (selects by masks of the word's sign: the compiler keeps them scalar)
+      const int sgn = raw >> 31;   // -1 for rows of k_new / v_new, else 0
+      const bool neg = sgn != 0;
+      const uint32_t idx = uint32_t(raw) & 0x7FFFFFFFu;
+      const bool inb = int(idx) <= cache_lim + (sgn & (fresh_lim - cache_lim));
+      auto where = [&](uint32_t i) __attribute__((always_inline)) -> const uint8_t* {
+        return c_src + (int64_t(sgn) & c_delta) + uint64_t(i) * row_bytes;
+      };
+      // fast path: a whole block, the next word inside the prompt's blocks, the
+      // cursor stays in its entry (c_fast > 0 implies !cdone)
+      if (c_fast > 0 && inb) {
+        const uint8_t* src = where(idx);
+        if constexpr (FUSED) dring = lane == (p & (kStages - 1)) ? dword : dring;
+        --c_fast;
+        --c_left;
+        c_lb += kKv / kBs;
+        c_ptr += (kKv / kBs) * TW;
+        load_bword(c_ptr);
+        const uint32_t off = neg ? off_n : off_c;
+        if (spread) {
+          cp_src = reinterpret_cast<uintptr_t>(src);
+          cp_dst = dst;
+          cp_stride = 1024;
+          cp_off = off;
+        } else {
+  #pragma unroll
+          for (int i = 0; i < LPW; ++i) copy16_to_lds(src, off, dst + i * 1024, i);
+        }
+        return true;
+      }
+      cp_src = reinterpret_cast<uintptr_t>(cache);
+      cp_dst = own_area;
+      cp_stride = 0;
+      cp_off = off_c;
+      if (cdone) {
+        if constexpr (FUSED) dring = lane == (p & (kStages - 1)) ? -1 : dring;
+        return false;
+      }
+      const int lb = c_lb, L = c_L;
+      const int key0 = lb * kBs;
+      // a block inside the prompt whose rows up to the prompt's end lie inside
+      // the source tensor (a partial block of k_new / v_new rows is not read
+      // past the prompt: the last request's end is the tensor's end)
+      bool valid = lb <= c_last;
+      if constexpr (FUSED) valid = valid && (neg ? int64_t(idx) + (L - 1 - key0) < a.total_rows : inb);
+      else valid = valid && inb;
+      const bool whole = valid && lb < c_whole;
+      const uint8_t* src = where(valid ? idx : 0u);
+      if constexpr (FUSED) dring = lane == (p & (kStages - 1)) ? (lb <= c_last ? dword : -1) : dring;
+      c_lb += kKv / kBs;
+      c_fast = max(0, c_fast - 1);
+      if (--c_left == 0) cursor_enter();
+      cursor_load();
+      if (whole) {   // wave-uniform: the whole block is valid
+        const uint32_t off = neg ? off_n : off_c;
+        if (spread) {
+          cp_src = reinterpret_cast<uintptr_t>(src);
+          cp_dst = dst;
+          cp_stride = 1024;
+          cp_off = off;
+        } else {
+  #pragma unroll
+          for (int i = 0; i < LPW; ++i) copy16_to_lds(src, off, dst + i * 1024, i);
+        }
+        return true;
+      }
+      const u32x4 zero{0, 0, 0, 0};
+      const uint32_t off_p =
+          (neg && valid) ? uint32_t(min(ckey, L - 1 - key0)) * row_bytes + uint32_t((lane >> 4) << 4) : off_c;
+  #pragma unroll
+      for (int i = 0; i < LPW; ++i) {
+        // (a missing block loads block 0 and discards it, so that every path
+        // through here waits for the memory operations issued before it)
+        u32x4 v = load16_now(src + off_p + 64 * i);
+        const bool ok = valid && key0 + ckey < L;
+        v = ok ? v : zero;
+        *reinterpret_cast<u32x4*>(lds + (dst - lds0) + i * 1024 + lane * 16) = v;
+      }
+      return false;
+      }
   };
   // End of a step: this wave's copies for the next steps have landed (the
   // copies issued in this step may still be in flight when `keep` says that
@@ -697,13 +833,17 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // Causal mask of the step starting at key k0: element e of accumulator h
     // holds key k0 + 32 h + (e / 8) 16 + half 8 + e % 8; the lane term moves to
     // the limit so that the per-element terms stay immediates.
+    // (each element is pinned after its select: otherwise the compiler keeps
+    // all 32 compare results live as lane masks in scalar registers)
     auto mask = [&](f32x16 (&sc)[2], int k0) __attribute__((always_inline)) {
       const int lim = qpos - k0 - half * 8;
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int e2 = 0; e2 < 16; ++e2)
+        for (int e2 = 0; e2 < 16; ++e2) {
           if (h * 32 + (e2 >> 3) * 16 + (e2 & 7) > lim) sc[h][e2] = -INFINITY;
+          asm volatile("" : "+v"(sc[h][e2]));
+        }
     };
     // Maximum of the row over a step's 64 keys (this lane's 32 and lane ^ 32's).
     auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) -> float {
@@ -932,8 +1072,81 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     auto touch_q = [&]() __attribute__((always_inline)) {
       touch_line(reinterpret_cast<const uint8_t*>(q_next) + half * 128, own_area);
     };
+    // FUSED: the keys of this entry's query rows are new keys of this call.
+    // Where this wave's block of step jj (ring position p) holds some of them
+    // (an entry's last steps), the wave writes those rows from the stage into
+    // the block's place in its cache (the destination recorded when the block
+    // was copied; -1 where the call writes nothing). A block the entry owns
+    // whole is written by LPW stores issued after the step's last copy
+    // (write_late): the step's barrier then leaves them in flight and the next
+    // step's barrier completes them. A block owned in part (a request's last
+    // rows, or tiles of fewer than 16 positions) is written at the step's
+    // start, before its copies (write_early).
+    constexpr int NST = LPW;        // store instructions per block
+    // the first step (from kbeg) that holds a key of the entry's own rows: the
+    // steps before it write nothing
+    const int own_j0 = (P + row0) / kKv - kbeg;
+    auto own_span = [&](int jj, int& key0, int& lo, int& hi) __attribute__((always_inline)) -> int {
+      key0 = ((kbeg + jj) * (kKv / kBs) + bs) * kBs;
+      lo = max(key0, P + row0);
+      hi = min(key0 + kBs, P + row0 + nvalid);
+      return __builtin_amdgcn_readlane(dring, p & (kStages - 1));
+    };
+    // The block as staged: lane l's 16 bytes at 1024 it + 16 l of its slot
+    // are the bytes it copied, chunk 4 it + l / 16 of key ckey, so they go to
+    // the same offset in the destination block as they came from (off_c).
+    auto own_chunk = [&](int it) __attribute__((always_inline)) -> u32x4 {
+      const uint32_t sb = slot0 - lds0 + uint32_t(p & (kStages - 1)) * stage_stride;
+      return *reinterpret_cast<const u32x4*>(lds + sb + it * 1024 + lane * 16);
+    };
+    auto own_dst = [&](int dstb) __attribute__((always_inline)) -> uint8_t* {
+      return reinterpret_cast<uint8_t*>(is_v ? a.vw : a.kw) + uint64_t(uint32_t(dstb)) * blk_bytes +
+             uint32_t(g) * (kBs * RB) + off_c;
+    };
+    auto write_early = [&](int jj) __attribute__((always_inline)) {
+      int key0, lo, hi;
+      const int dstb = own_span(jj, key0, lo, hi);
+      if (uint32_t(dstb) >= uint32_t(a.num_blocks) || lo >= hi || (lo == key0 && hi == key0 + kBs)) return;
+      u32x4 t[LPW];
+#pragma unroll
+      for (int it = 0; it < LPW; ++it) t[it] = own_chunk(it);
+      uint8_t* dp = own_dst(dstb);
+      const bool mine = key0 + ckey >= lo && key0 + ckey < hi;
+#pragma unroll
+      for (int it = 0; it < LPW; ++it)
+        if (mine) *reinterpret_cast<u32x4*>(dp + 64 * it) = t[it];
+    };
+    auto write_late = [&](int jj) __attribute__((always_inline)) -> bool {
+      int key0, lo, hi;
+      const int dstb = own_span(jj, key0, lo, hi);
+      if (uint32_t(dstb) >= uint32_t(a.num_blocks) || lo != key0 || hi != key0 + kBs) return false;
+      u32x4 t[LPW];
+#pragma unroll
+      for (int it = 0; it < LPW; ++it) t[it] = own_chunk(it);
+      uint8_t* dp = own_dst(dstb);
+#pragma unroll
+      for (int it = 0; it < LPW; ++it) {
+        // (a store of more than 8 bytes reads its data registers after issue:
+        // wait states before an instruction may write them)
+        asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" :: "v"(dp + 64 * it), "v"(t[it]) : "memory");
+      }
+      return true;
+    };
+    // The step barrier after write_late's stores: they stay in flight with
+    // the step's copies.
+    auto step_barrier_w = [&](bool keep, bool late) __attribute__((always_inline)) {
+      if (keep && late) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(LPW + NST));
+      else if (keep) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(LPW));
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    };
     // Step j < nsteps - 1 at ring position p: current S in sc, next S into sn.
     auto step = [&](int j, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
+      if constexpr (FUSED) {
+        if (j >= own_j0) write_early(j);
+      }
       bf16x8 kf[3], vf[3];
 #pragma unroll
       for (int i = 0; i < 3; ++i) kf[i] = rdk(kbase(p + 1), i);
@@ -946,7 +1159,8 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, kEarly, 2 * KS, true);
       if (j + 1 >= n_full) mask(sn, (kbeg + j + 1) * kKv);
       mx = phase_b(vbase(p), vf, pb, sn);
-      step_barrier(direct);
+      if (FUSED && j >= own_j0) step_barrier_w(direct, write_late(j));
+      else step_barrier(direct);
       ++p;
     };
     int j = 0;
@@ -964,12 +1178,16 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     {   // the entry's last step: P and PV only. qf is no longer needed: the
         // next entry's Q is loaded now, ahead of this step's table word and
         // copies, so that this step's barrier completes it.
+      if constexpr (FUSED) {
+        if (last >= own_j0) write_early(last);
+      }
       load_q(q_next);
       load_desc(e + grid);
       const bool direct = issue(p + kAhead, true);
       rebase(sa);
       phase_last(vbase(p), sa);
-      step_barrier(direct);
+      if (FUSED && last >= own_j0) step_barrier_w(direct, write_late(last));
+      else step_barrier(direct);
       ++p;
     }
 
@@ -1141,9 +1359,11 @@ cw_status check_attn(const char* what, const void* q, const void* k_cache, const
                      const int32_t* prefix_len_host, int32_t batch, int32_t num_q_heads,
                      int32_t num_kv_heads, int32_t head_dim, int32_t block_size, int32_t num_blocks,
                      float softmax_scale, const int32_t* plan_host, const int32_t* plan_dev, const void* out,
-                     AttnLaunch* L) {
+                     AttnLaunch* L, const int32_t* append_bt_host = nullptr) {
   const std::string w(what);
-  if (!q || !k_cache || !v_cache || !block_table || !cu_suffix_dev || !prefix_len_dev || !out)
+  // the fused call reads no device block table or offsets: its plan carries them
+  const bool fused = append_bt_host != nullptr;
+  if (!q || !k_cache || !v_cache || !out || (!fused && (!block_table || !cu_suffix_dev || !prefix_len_dev)))
     return cw::fail(CW_EINVAL, w + ": a required pointer is NULL");
   if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0)
     return cw::fail(CW_EINVAL, w + ": num_q_heads must be a positive multiple of num_kv_heads");
@@ -1159,13 +1379,19 @@ cw_status check_attn(const char* what, const void* q, const void* k_cache, const
   if (st != CW_OK) return st;
   AttnArgs& a = L->args;
   st = cw::check_plan_header(what, plan_host, cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads,
-                             head_dim, &L->grid, &L->splits, &a.fp_lo, &a.fp_hi, &a.num_entries);
+                             head_dim, &L->grid, &L->splits, &a.fp_lo, &a.fp_hi, &a.num_entries, append_bt_host,
+                             bt_stride, num_blocks);
   if (st != CW_OK) return st;
   if (L->grid > 0 && !plan_dev) return cw::fail(CW_EINVAL, w + ": plan_dev is required");
   a.q = static_cast<const uint16_t*>(q);
   a.kc = static_cast<const uint16_t*>(k_cache);
   a.vc = static_cast<const uint16_t*>(v_cache);
-  a.bt = block_table;
+  a.bt = fused ? plan_dev + plan_host[cw::kHdrTable] : block_table;
+  a.kn = nullptr;
+  a.vn = nullptr;
+  a.kw = nullptr;
+  a.vw = nullptr;
+  a.total_rows = 0;
   a.plan = plan_dev;
   a.out = static_cast<uint16_t*>(const_cast<void*>(out));
   a.part_o = nullptr;
@@ -1181,14 +1407,14 @@ cw_status check_attn(const char* what, const void* q, const void* k_cache, const
   return CW_OK;
 }
 
-template <bool SPLIT>
+template <bool SPLIT, bool FUSED = false>
 void launch_attn(int head_dim, const AttnLaunch& L, hipStream_t s) {
   if (head_dim == 128)
-    hipLaunchKernelGGL((suffix_prefill_attn_kernel<128, SPLIT>), dim3(unsigned(L.grid)), dim3(kAttnThreads), 0, s,
-                       L.args);
+    hipLaunchKernelGGL((suffix_prefill_attn_kernel<128, SPLIT, FUSED>), dim3(unsigned(L.grid)), dim3(kAttnThreads),
+                       0, s, L.args);
   else
-    hipLaunchKernelGGL((suffix_prefill_attn_kernel<64, SPLIT>), dim3(unsigned(L.grid)), dim3(kAttnThreads), 0, s,
-                       L.args);
+    hipLaunchKernelGGL((suffix_prefill_attn_kernel<64, SPLIT, FUSED>), dim3(unsigned(L.grid)), dim3(kAttnThreads),
+                       0, s, L.args);
 }
 
 // Workspace of the split path: part_o [splits][rows][D] fp32, then part_lse
@@ -1228,6 +1454,33 @@ extern "C" cw_status cw_suffix_prefill_attn(const void* q, const void* k_cache, 
   if (L.rows == 0 || L.grid == 0) return cw::ok();
   launch_attn<false>(head_dim, L, static_cast<hipStream_t>(stream));
   return check_launch("suffix_prefill_attn launch");
+}
+
+extern "C" cw_status cw_suffix_prefill_append_attn(const void* q, const void* k_new, const void* v_new,
+                                                   void* k_cache, void* v_cache, const int32_t* block_table_host,
+                                                   int32_t bt_stride, const int32_t* cu_suffix_host,
+                                                   const int32_t* prefix_len_host, int32_t batch,
+                                                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                                   int32_t block_size, int32_t num_blocks, float softmax_scale,
+                                                   const int32_t* plan_host, const int32_t* plan_dev, void* out,
+                                                   void* stream) {
+  if (!k_new || !v_new || !block_table_host)
+    return cw::fail(CW_EINVAL, "suffix_prefill_append_attn: a required pointer is NULL");
+  AttnLaunch L;
+  cw_status st = check_attn("suffix_prefill_append_attn", q, k_cache, v_cache, nullptr, bt_stride, nullptr, nullptr,
+                            cu_suffix_host, prefix_len_host, batch, num_q_heads, num_kv_heads, head_dim, block_size,
+                            num_blocks, softmax_scale, plan_host, plan_dev, out, &L, block_table_host);
+  if (st != CW_OK) return st;
+  if (L.rows == 0 || L.grid == 0) return cw::ok();
+  if (num_blocks > cw::kMaxAppendBlocks)
+    return cw::fail(CW_EUNSUPPORTED, "suffix_prefill_append_attn: num_blocks must be below 2^27");
+  L.args.total_rows = int32_t(L.rows);
+  L.args.kn = static_cast<const uint16_t*>(k_new);
+  L.args.vn = static_cast<const uint16_t*>(v_new);
+  L.args.kw = static_cast<uint16_t*>(k_cache);
+  L.args.vw = static_cast<uint16_t*>(v_cache);
+  launch_attn<false, true>(head_dim, L, static_cast<hipStream_t>(stream));
+  return check_launch("suffix_prefill_append_attn launch");
 }
 
 extern "C" int64_t cw_suffix_prefill_split_workspace_bytes(int64_t total_rows, int32_t num_q_heads,

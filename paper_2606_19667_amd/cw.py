@@ -30,6 +30,7 @@ TILE_ROWS = 256    # packed query rows (heads x positions) of one attention tile
 PLAN_HEADER = 16   # int32 words of a plan's header, then entries of PLAN_ENTRY words
 PLAN_ENTRY = 16
 HDR_ENTRIES, HDR_GRID, HDR_SPLITS, HDR_QUEUE_LEN, HDR_WORK = 1, 4, 5, 11, 12
+HDR_TABLE, HDR_TABLE_STRIDE, HDR_NUM_BLOCKS = 13, 14, 15
 ENT_R, ENT_G, ENT_ROW0, ENT_NVALID, ENT_CU0, ENT_P, ENT_L, ENT_KBEG, ENT_KEND, ENT_SPLIT = range(10)
 
 _i32 = ctypes.c_int32
@@ -74,6 +75,11 @@ def _load() -> ctypes.CDLL:
         "cw_suffix_prefill_attn": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
                                           _i32, _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp,
                                           _vp, _vp]),
+        "cw_suffix_prefill_append_plan_words": (_i64, [_pi32, _pi32, _i32, _i32, _i32, _i32, _i32]),
+        "cw_suffix_prefill_append_plan": (_i32, [_pi32, _pi32, _pi32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                                 _pi32, _i64]),
+        "cw_suffix_prefill_append_attn": (_i32, [_vp, _vp, _vp, _vp, _vp, _pi32, _i32, _pi32, _pi32, _i32,
+                                                 _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp, _vp, _vp]),
         "cw_suffix_prefill_split_workspace_bytes": (_i64, [_i64, _i32, _i32, _i32]),
         "cw_suffix_prefill_attn_split": (_i32, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _pi32, _pi32,
                                                 _i32, _i32, _i32, _i32, _i32, _i32, _f32, _pi32, _vp,
@@ -108,7 +114,8 @@ EXPORTED = ("cw_abi_version", "cw_last_error", "cw_block_hashes", "cw_pool_creat
             "cw_pool_destroy", "cw_pool_clone", "cw_pool_num_free", "cw_prefix_match",
             "cw_pool_alloc", "cw_pool_commit", "cw_pool_release", "cw_schedule_batch",
             "cw_release_batch", "cw_kv_append", "cw_suffix_prefill_plan_words",
-            "cw_suffix_prefill_plan", "cw_suffix_prefill_attn",
+            "cw_suffix_prefill_plan", "cw_suffix_prefill_attn", "cw_suffix_prefill_append_plan_words",
+            "cw_suffix_prefill_append_plan", "cw_suffix_prefill_append_attn",
             "cw_suffix_prefill_split_workspace_bytes", "cw_suffix_prefill_attn_split", "cw_lse_merge",
             "cw_noalloc_scratch_bytes", "cw_suffix_prefill_attn_split_noalloc",
             "cw_tree_create", "cw_tree_destroy", "cw_tree_num_nodes", "cw_tree_insert",
@@ -325,7 +332,37 @@ def suffix_prefill_plan(cu_suffix, prefix_len, num_q_heads: int, num_kv_heads: i
 def plan_entries(plan: np.ndarray) -> np.ndarray:
     """The entries of a plan as an [n, PLAN_ENTRY] view (padding included:
     entries with request -1 end a queue)."""
-    return plan[PLAN_HEADER:].reshape(-1, PLAN_ENTRY)
+    n = int(plan[HDR_ENTRIES])
+    return plan[PLAN_HEADER:PLAN_HEADER + n * PLAN_ENTRY].reshape(-1, PLAN_ENTRY)
+
+
+def suffix_prefill_append_plan(cu_suffix, prefix_len, block_table, num_q_heads: int, num_kv_heads: int,
+                               head_dim: int, num_blocks: int) -> np.ndarray:
+    """cw_suffix_prefill_append_plan: the plan of the fused append + attention
+    call (header, entries, then the (source, destination) table)."""
+    cu = _i32_array(cu_suffix, "cu_suffix")
+    plen = _i32_array(prefix_len, "prefix_len")
+    bt = _i32_array(block_table, "block_table")
+    if bt.ndim != 2 or bt.shape[0] != len(plen):
+        raise ValueError("block_table must be [batch, stride]")
+    B = len(plen)
+    words = int(_lib.cw_suffix_prefill_append_plan_words(_ptr(cu, ctypes.c_int32), _ptr(plen, ctypes.c_int32),
+                                                         bt.shape[1], B, num_q_heads, num_kv_heads, head_dim))
+    if words < 0:
+        _check(words)
+    plan = np.zeros(words, dtype=np.int32)
+    _check(_lib.cw_suffix_prefill_append_plan(_ptr(cu, ctypes.c_int32), _ptr(plen, ctypes.c_int32),
+                                              _ptr(bt, ctypes.c_int32), bt.shape[1], B, num_q_heads, num_kv_heads,
+                                              head_dim, int(num_blocks), _ptr(plan, ctypes.c_int32), len(plan)))
+    return plan
+
+
+def append_table(plan: np.ndarray) -> np.ndarray:
+    """The (source, destination) table of a fused plan as [batch, stride, 2]."""
+    t0, stride = int(plan[HDR_TABLE]), int(plan[HDR_TABLE_STRIDE])
+    if t0 == 0:
+        raise ValueError("not a plan of cw_suffix_prefill_append_plan")
+    return plan[t0:].reshape(-1, stride, 2)
 
 
 # ---------------------------------------------------------------- device calls
@@ -391,6 +428,7 @@ class BatchMeta:
         self.device = device
         self.bt = self.cu = self.plen = self.plan = None
         self._split_plans = {}
+        self._append_plans = {}
         if device is not None:
             self.bt = torch.from_numpy(self.bt_host).to(device)
             self.cu = torch.from_numpy(self.cu_host).to(device)
@@ -421,6 +459,16 @@ class BatchMeta:
             self._split_plans[num_splits] = (ph, pd)
         return self._split_plans[num_splits]
 
+    def append_plan(self, num_blocks: int):
+        """(host plan, device plan) of the fused append + attention call for a
+        pool of `num_blocks` blocks."""
+        if num_blocks not in self._append_plans:
+            ph = suffix_prefill_append_plan(self.cu_host, self.plen_host, self.bt_host, self.num_q_heads,
+                                            self.num_kv_heads, self.head_dim, num_blocks)
+            pd = torch.from_numpy(ph).to(self.device) if self.device is not None else None
+            self._append_plans[num_blocks] = (ph, pd)
+        return self._append_plans[num_blocks]
+
     def _hp(self, a):
         return _ptr(a, ctypes.c_int32)
 
@@ -432,6 +480,8 @@ class BatchMeta:
                  ("prefix_len", self.plen, self.plen_host), ("plan", self.plan, self.plan_host)]
         for n, (ph, pd) in self._split_plans.items():
             pairs.append((f"plan ({n} splits)", pd, ph))
+        for n, (ph, pd) in self._append_plans.items():
+            pairs.append((f"append plan ({n} blocks)", pd, ph))
         _check_copies(pairs)
 
 
@@ -519,6 +569,35 @@ def suffix_prefill_attn(meta: BatchMeta, q: torch.Tensor, k_cache: torch.Tensor,
         meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch, hq, hkv, D, BLOCK_SIZE,
         k_cache.shape[0], float(softmax_scale), meta._hp(meta.plan_host), _dev(meta.plan, torch.int32, "plan"),
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out
+
+
+def suffix_prefill_append_attn(meta: BatchMeta, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                               k_cache: torch.Tensor, v_cache: torch.Tensor, softmax_scale: float,
+                               out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """cw_suffix_prefill_append_attn: cw_kv_append and cw_suffix_prefill_attn in
+    one launch (same cache image and output); returns out [total_s, Hq, D]."""
+    hq, hkv, D = meta.num_q_heads, meta.num_kv_heads, meta.head_dim
+    if tuple(q.shape) != (meta.total_rows, hq, D):
+        raise ValueError(f"q must be [{meta.total_rows}, {hq}, {D}], got {tuple(q.shape)}")
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        if tuple(t.shape) != (meta.total_rows, hkv, D):
+            raise ValueError(f"{name} must be [{meta.total_rows}, {hkv}, {D}], got {tuple(t.shape)}")
+    if not _cache_shapes_ok(k_cache, v_cache, hkv, D):
+        raise ValueError("k_cache and v_cache must both be [num_blocks, Hkv, 16, D]")
+    if out is None:
+        out = torch.empty_like(q)
+    elif tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must have q's shape")
+    ph, pd = meta.append_plan(int(k_cache.shape[0]))
+    if DEBUG_CHECK_COPIES:
+        meta.check_device_copies()
+    _check(_lib.cw_suffix_prefill_append_attn(
+        _dev(q, torch.bfloat16, "q"), _dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
+        _dev(k_cache, torch.bfloat16, "k_cache"), _dev(v_cache, torch.bfloat16, "v_cache"),
+        meta._hp(meta.bt_host), meta.bt_stride, meta._hp(meta.cu_host), meta._hp(meta.plen_host), meta.batch,
+        hq, hkv, D, BLOCK_SIZE, k_cache.shape[0], float(softmax_scale), meta._hp(ph),
+        _dev(pd, torch.int32, "plan"), _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
 
@@ -629,11 +708,14 @@ class BatchRunner:
     asynchronous), the device copies, and the C entry points with their
     arguments converted once. Each schedule() / upload() / launch call is then
     one ctypes call on cached arguments; the C library still validates every
-    call.
+    call. With fused=True the plan is the fused call's
+    (cw_suffix_prefill_append_plan, built for the pool of the caches given to
+    bind(), which must come first) and append_attention() runs the append and
+    the attention in one launch.
     """
 
     def __init__(self, prompts, bt_stride: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
-                 block_size: int = BLOCK_SIZE, device="cuda"):
+                 block_size: int = BLOCK_SIZE, device="cuda", fused: bool = False):
         toks = [_i32_array(p, "tokens") for p in prompts]
         self.batch = B = len(toks)
         self.bt_stride = int(bt_stride)
@@ -647,8 +729,14 @@ class BatchRunner:
         max_cu = np.zeros(B + 1, dtype=np.int32)
         max_cu[1:] = np.cumsum(np.diff(self.cu_tokens))
         zero = np.zeros(B, dtype=np.int32)
-        words = int(_lib.cw_suffix_prefill_plan_words(_ptr(max_cu, ctypes.c_int32), _ptr(zero, ctypes.c_int32),
-                                                      B, num_q_heads, num_kv_heads, head_dim, 1))
+        self.fused = bool(fused)
+        if self.fused:
+            words = int(_lib.cw_suffix_prefill_append_plan_words(
+                _ptr(max_cu, ctypes.c_int32), _ptr(zero, ctypes.c_int32), self.bt_stride, B, num_q_heads,
+                num_kv_heads, head_dim))
+        else:
+            words = int(_lib.cw_suffix_prefill_plan_words(_ptr(max_cu, ctypes.c_int32), _ptr(zero, ctypes.c_int32),
+                                                          B, num_q_heads, num_kv_heads, head_dim, 1))
         if words < 0:
             _check(words)
         # queues of uneven entry counts pad to the longest: leave room for that
@@ -682,6 +770,8 @@ class BatchRunner:
                    "cu": p32(self.cu_host), "pl": p32(self.plen_host), "plan": p32(self.plan_host)}
         self._append_args = None
         self._attn_args = None
+        self._fused_args = None
+        self._num_blocks = None
 
     @property
     def total_rows(self) -> int:
@@ -689,6 +779,14 @@ class BatchRunner:
 
     def _plan(self) -> None:
         p = self._p
+        if self.fused:
+            if self._num_blocks is None:
+                raise RuntimeError("a fused runner needs bind() before its first schedule")
+            _check(_lib.cw_suffix_prefill_append_plan(p["cu"], p["pl"], p["bt"], self.bt_stride, self.batch,
+                                                      self.num_q_heads, self.num_kv_heads, self.head_dim,
+                                                      self._num_blocks, p["plan"], self.plan_capacity))
+            self.plan_words = int(self.plan_host[HDR_TABLE]) + 2 * self.batch * self.bt_stride
+            return
         _check(_lib.cw_suffix_prefill_plan(p["cu"], p["pl"], self.batch, self.num_q_heads, self.num_kv_heads,
                                            self.head_dim, 1, p["plan"], self.plan_capacity))
         self.plan_words = PLAN_HEADER + PLAN_ENTRY * int(self.plan_host[HDR_ENTRIES])
@@ -736,6 +834,11 @@ class BatchRunner:
                            self.cu.data_ptr(), self.plen.data_ptr(), p["cu"], p["pl"], self.batch, hq, hkv, D,
                            BLOCK_SIZE, k_cache.shape[0], float(softmax_scale), p["plan"], self.plan.data_ptr(),
                            out.data_ptr(), s]
+        self._fused_args = [q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                            p["bt"], self.bt_stride, p["cu"], p["pl"], self.batch, hq, hkv, D, BLOCK_SIZE,
+                            k_cache.shape[0], float(softmax_scale), p["plan"], self.plan.data_ptr(), out.data_ptr(),
+                            s]
+        self._num_blocks = int(k_cache.shape[0])
         self._rows = (q.shape[0], k_new.shape[0], v_new.shape[0], out.shape[0])
 
     def check_device_copies(self) -> None:
@@ -752,11 +855,23 @@ class BatchRunner:
         _check(_lib.cw_kv_append(*self._append_args))
 
     def attention(self) -> None:
+        if self.fused:
+            raise RuntimeError("a fused runner's plan is for append_attention()")
         if any(n != self.total_rows for n in self._rows):
             raise ValueError("bound tensors do not match the scheduled suffix rows")
         if DEBUG_CHECK_COPIES:
             self.check_device_copies()
         _check(_lib.cw_suffix_prefill_attn(*self._attn_args))
+
+    def append_attention(self) -> None:
+        """cw_suffix_prefill_append_attn: the append and the attention in one launch."""
+        if not self.fused:
+            raise RuntimeError("append_attention() needs a runner built with fused=True")
+        if any(n != self.total_rows for n in self._rows):
+            raise ValueError("bound tensors do not match the scheduled suffix rows")
+        if DEBUG_CHECK_COPIES:
+            self.check_device_copies()
+        _check(_lib.cw_suffix_prefill_append_attn(*self._fused_args))
 
 
 # ---------------------------------------------------------------- measurement aid

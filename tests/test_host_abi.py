@@ -522,3 +522,119 @@ def test_debug_check_of_device_copies():
     meta.plan = None
     with pytest.raises(ValueError, match="no device copy"):
         meta.check_device_copies()
+
+
+# ------------------------------------------------------------------ fused append + attention plan
+def _expected_append_table(cu, plen, bt, nb):
+    """The (source, destination) words by their definition, from the batch
+    description alone: a request's own suffix blocks are read from its rows and
+    written to their block; a prefix block that is a full suffix block of the
+    batch is read from that block's rows; other in-pool blocks from the cache."""
+    B, stride = bt.shape
+    fresh = {}
+    for r in range(B):
+        P, L = plen[r], plen[r] + cu[r + 1] - cu[r]
+        for j in range(P // 16, -(-L // 16)):
+            if 0 <= bt[r, j] < nb:
+                fresh[int(bt[r, j])] = cu[r] + 16 * j - P if 16 * (j + 1) <= L else None
+    rows = lambda R: int(np.array([0x80000000 | int(R)], np.uint32).view(np.int32)[0])   # noqa: E731
+    t = np.full((B, stride, 2), -1, np.int64)
+    for r in range(B):
+        P, L = plen[r], plen[r] + cu[r + 1] - cu[r]
+        for j in range(-(-L // 16)):
+            b = int(bt[r, j])
+            if not 0 <= b < nb:
+                continue
+            if j >= P // 16:
+                t[r, j] = (rows(cu[r] + 16 * j - P), b)
+            else:
+                t[r, j, 0] = rows(fresh[b]) if b in fresh else 16 * b
+    return t
+
+
+def _random_batch(rng, B=6, stride=12, nb=200):
+    S = rng.integers(0, 60, size=B)
+    P = 16 * rng.integers(0, 4, size=B)
+    cu = np.concatenate([[0], np.cumsum(S)]).astype(np.int32)
+    bt = rng.permutation(nb)[:B * stride].reshape(B, stride).astype(np.int32)
+    return cu, P.astype(np.int32), bt
+
+
+def test_append_plan_table_matches_its_definition():
+    rng = np.random.default_rng(3)
+    for trial in range(20):
+        cu, P, bt = _random_batch(rng)
+        nb = 200
+        # alias some prefix blocks to full suffix blocks of the batch, and put
+        # out-of-pool entries in prefix and suffix blocks
+        full = [(r, j) for r in range(len(P)) for j in range(P[r] // 16, (P[r] + cu[r + 1] - cu[r]) // 16)]
+        pre = [(r, j) for r in range(len(P)) for j in range(P[r] // 16)]
+        for (r, j), (r2, j2) in zip(pre[:2], full[::-1][:2]):
+            if r != r2:
+                bt[r, j] = bt[r2, j2]
+        if trial % 3 == 0 and pre:
+            bt[pre[-1]] = -1
+        if trial % 4 == 1 and full:
+            bt[full[0]] = nb + 3
+        plan = cw.suffix_prefill_append_plan(cu, P, bt, 8, 2, 128, nb)
+        assert plan[cw.HDR_TABLE] > 0 and plan[cw.HDR_TABLE_STRIDE] == bt.shape[1] and plan[cw.HDR_NUM_BLOCKS] == nb
+        np.testing.assert_array_equal(cw.append_table(plan), _expected_append_table(cu, P, bt, nb))
+        # the entries are those of the unsplit plan
+        np.testing.assert_array_equal(cw.plan_entries(plan)[:, :12],
+                                      cw.plan_entries(cw.suffix_prefill_plan(cu, P, 8, 2, 128))[:, :12])
+
+
+def test_append_plan_refuses_racing_or_mixed_blocks():
+    cu = np.array([0, 40, 70], np.int32)
+    P = np.array([32, 16], np.int32)
+    bt = np.arange(2 * 8, dtype=np.int32).reshape(2, 8) + 10
+    bt2 = bt.copy()
+    bt2[1, 2] = bt2[0, 3]                       # a suffix block named twice
+    with pytest.raises(cw.CwError) as ei:
+        cw.suffix_prefill_append_plan(cu, P, bt2, 8, 2, 128, 100)
+    assert ei.value.status == cw.CW_EINVAL
+    bt3 = bt.copy()
+    bt3[1, 0] = bt3[0, 4]                       # request 0's partial last block (keys 64..71)
+    with pytest.raises(cw.CwError) as ei:
+        cw.suffix_prefill_append_plan(cu, P, bt3, 8, 2, 128, 100)
+    assert ei.value.status == cw.CW_EUNSUPPORTED
+    bt4 = bt.copy()
+    bt4[1, 0] = bt4[0, 3]                       # a full suffix block: allowed, read from its rows
+    t = cw.append_table(cw.suffix_prefill_append_plan(cu, P, bt4, 8, 2, 128, 100))
+    assert tuple(t[1, 0]) == (int(np.array([0x80000000 | 16], np.uint32).view(np.int32)[0]), -1)
+    with pytest.raises(cw.CwError):
+        cw.suffix_prefill_append_plan(cu, P, bt, 8, 2, 128, 0)        # num_blocks
+    with pytest.raises(cw.CwError):
+        cw.suffix_prefill_append_plan(cu, P, bt[:, :4], 8, 2, 128, 100)   # stride too small for request 0
+
+
+def _fused_call(cu, plen, bt, plan, hq=8, hkv=2, d=128, nb=100, bt_call=None):
+    cu_a, cu_p = _arr(cu)
+    pl_a, pl_p = _arr(plen)
+    b = np.ascontiguousarray(bt if bt_call is None else bt_call, np.int32)
+    bp = b.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    plan = np.ascontiguousarray(plan, np.int32)
+    pp = plan.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    d_ = _dummy()
+    return cw.lib().cw_suffix_prefill_append_attn(d_, d_, d_, d_, d_, bp, b.shape[1], cu_p, pl_p, len(plen), hq, hkv,
+                                                  d, 16, nb, 0.1, pp, d_, d_, None)
+
+
+def test_fused_call_validates_its_plan_before_launch():
+    E = cw.CW_EINVAL
+    cu = np.array([0, 40, 70], np.int32)
+    P = np.array([32, 16], np.int32)
+    bt = np.arange(2 * 8, dtype=np.int32).reshape(2, 8) + 10
+    fused = cw.suffix_prefill_append_plan(cu, P, bt, 8, 2, 128, 100)
+    plain = cw.suffix_prefill_plan(cu, P, 8, 2, 128)
+    assert _fused_call(cu, P, bt, plain) == E                          # no table
+    assert "append table" in cw.last_error()
+    other = bt.copy()
+    other[0, 0] = 99
+    assert _fused_call(cu, P, bt, fused, bt_call=other) == E           # another block table
+    assert _fused_call(cu, P, bt, fused, nb=101) == E                  # another pool size
+    assert _fused_call(cu, P, bt, fused, hq=16) == E                   # another head count
+    assert _attn(cu, P, hq=8, hkv=2, stride=8, plan=fused) == E        # the plain call refuses it
+    assert "cw_suffix_prefill_append_attn" in cw.last_error()
+    assert _fused_call([0, 0], [16], bt[:1], cw.suffix_prefill_append_plan([0, 0], [16], bt[:1], 8, 2, 128, 100)) \
+        == cw.CW_OK                                                    # nothing to do: no launch
