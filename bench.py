@@ -71,9 +71,10 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_19667_amd", "csrc", "cw_kernels.h
 
 
 def counted_traffic(workload: str):
-    """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE /
-    WRITE_SIZE summary (already scaled by the copy calibration), or None when
-    that summary is for another workload or an older kernel source."""
+    """HBM bytes per launch of the fused append + attention kernel from the
+    committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary (already scaled by the
+    copy calibration), or None when that summary is for another workload or an
+    older kernel source."""
     import hashlib
     try:
         fields = dict(line.split(": ", 1) for line in open(PROFILE).read().splitlines()
@@ -83,7 +84,7 @@ def counted_traffic(workload: str):
         return None
     if workload != "llama8b-trace-b16" or fields.get("kernel_source_sha256_16") != src:
         return None
-    return int(fields["attention_traffic_bytes"])
+    return int(fields["append_attention_traffic_bytes"])
 
 
 def make_workload(name: str, seed: int):
