@@ -577,7 +577,7 @@ def main() -> int:
     achieved = flops / (fused_ms * 1e-3) / 1e12
     mfma_flops = executed_mfma_flops(sched.cu_suffix, P, hq, hkv, D)
     res = {
-        "metric": "suffix-prefill attention TFLOP/s (whole step: schedule + kv_append + attention)",
+        "metric": "suffix-prefill attention TFLOP/s (whole step: schedule + KV append + attention)",
         "value": round(flops / (ms_per_step * 1e-3) / 1e12, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,

@@ -11,8 +11,10 @@ assembly from each such load and reports any instruction that touches its
 destination registers before a covering wait.
 
 A load counts as untracked when it sits in an inline-asm block without a wait
-of its own; `s_waitcnt vmcnt(k)` covers a load on a path where at least k
-memory instructions were issued after it.
+of its own; `s_waitcnt vmcnt(k)` covers a vector load on a path where at least
+k memory instructions were issued after it. Untracked scalar loads
+(`s_load_dword*`, SGPR destinations) are covered only by an `s_waitcnt` with
+`lgkmcnt(0)` (scalar loads return out of order).
 
 Paths follow branch conditions in one form the compiler uses for wave-uniform
 if/else: an if/else becomes two sequential `if`s on one SGPR-pair flag F set
@@ -28,6 +30,8 @@ import re
 
 _VMEM = re.compile(r'^(global_|buffer_|flat_|scratch_)')
 _LOAD = re.compile(r'^global_load_dword(x[234])?\s')
+_SLOAD = re.compile(r'^s_load_dword(x[248])?\s')
+_SREG = re.compile(r'\bs\[(\d+):(\d+)\]|\bs(\d+)\b')
 _LABEL = re.compile(r'^(\.?[\w.$]+):')
 _VREG = re.compile(r'\bv\[(\d+):(\d+)\]|\bv(\d+)\b')
 
@@ -43,9 +47,23 @@ def vregs(text: str) -> set[int]:
     return out
 
 
+def sregs(text: str) -> set[int]:
+    """SGPR numbers named in an instruction's operands."""
+    out: set[int] = set()
+    parts = text.split(None, 1)
+    if len(parts) < 2:
+        return out
+    for m in _SREG.finditer(parts[1]):
+        if m.group(3):
+            out.add(int(m.group(3)))
+        else:
+            out.update(range(int(m.group(1)), int(m.group(2)) + 1))
+    return out
+
+
 def parse(lines: list[str]):
     """Instructions (text), label -> instruction index, and the indices of
-    untracked loads."""
+    untracked loads (vector and scalar)."""
     insts: list[str] = []
     labels: dict[str, int] = {}
     untracked: list[int] = []
@@ -58,7 +76,7 @@ def parse(lines: list[str]):
             if block is not None:
                 texts = [insts[i] for i in block]
                 if not any(t.startswith('s_waitcnt') for t in texts):
-                    untracked.extend(i for i in block if _LOAD.match(insts[i]))
+                    untracked.extend(i for i in block if _LOAD.match(insts[i]) or _SLOAD.match(insts[i]))
             block = None
             continue
         text = raw.split(';')[0].strip()
@@ -202,7 +220,10 @@ def hazards(lines: list[str]) -> list[tuple[str, str]]:
     facts = _entry_facts(insts, labels)
     found = []
     for li in loads:
-        dst = vregs(insts[li].split()[1].rstrip(','))
+        scalar = bool(_SLOAD.match(insts[li]))
+        first = insts[li].split()[1].rstrip(',')
+        dst = sregs('x ' + first) if scalar else vregs(first)
+        touches = sregs if scalar else vregs
         if facts[li] is None:
             continue
         seen = set()
@@ -220,12 +241,16 @@ def hazards(lines: list[str]) -> list[tuple[str, str]]:
             text = insts[i]
             op = text.split()[0]
             if op == 's_waitcnt':
-                m = re.search(r'vmcnt\((\d+)\)', text)
-                if m and int(m.group(1)) <= younger:
-                    continue
-            elif op == 's_barrier':
+                if scalar:
+                    if re.search(r'lgkmcnt\(0\)', text):
+                        continue
+                else:
+                    m = re.search(r'vmcnt\((\d+)\)', text)
+                    if m and int(m.group(1)) <= younger:
+                        continue
+            elif op == 's_barrier' and not scalar:
                 continue
-            elif vregs(text) & dst:
+            elif touches(text) & dst:
                 found.append((insts[li], text))
                 continue
             nxt = younger + (1 if _VMEM.match(text) else 0)

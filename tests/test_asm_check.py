@@ -78,3 +78,26 @@ def test_flag_set_to_a_constant_is_known():
     # the other constant: the use follows the load
     assert _hazards(body.replace("s_mov_b64 s[12:13], 0\n", "s_mov_b64 s[12:13], -1\n", 1).replace(
         "\ts_mov_b64 s[12:13], -1\n\ts_cbranch_scc1", "\ts_mov_b64 s[12:13], 0\n\ts_cbranch_scc1"))
+
+
+SLOAD = "\t;;#ASMSTART\n\ts_load_dwordx2 s[12:13], s[4:5], 0x0\n\t;;#ASMEND\n"
+
+
+def test_scalar_load_destination_use_before_lgkmcnt0_is_reported():
+    # a read (copy) and a write of the destination before the wait
+    assert _hazards(SLOAD + "\ts_mov_b32 s20, s13\n\ts_waitcnt lgkmcnt(0)\n")
+    assert _hazards(SLOAD + "\ts_add_u32 s12, s12, 4\n")
+    # a vector wait, or a partial lgkm wait, does not cover a scalar load
+    assert _hazards(SLOAD + "\ts_waitcnt vmcnt(0)\n\tv_mov_b32_e32 v2, s12\n")
+    assert _hazards(SLOAD + "\ts_waitcnt lgkmcnt(1)\n\tv_mov_b32_e32 v2, s12\n")
+    # nor does a barrier without the wait
+    assert _hazards(SLOAD + "\ts_barrier\n\tv_mov_b32_e32 v2, s12\n")
+
+
+def test_scalar_load_covered_by_lgkmcnt0_is_clear():
+    assert not _hazards(SLOAD + "\ts_mov_b32 s20, s14\n\ts_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier\n"
+                                "\tv_mov_b32_e32 v2, s12\n\ts_add_u32 s12, s12, 4\n")
+    # other registers may be used meanwhile, and the paths all pass the wait
+    body = SLOAD + ("\ts_cbranch_scc1 .LBB0_2\n\ts_mov_b32 s30, 1\n.LBB0_2:\n"
+                    "\ts_waitcnt lgkmcnt(0)\n\ts_mov_b32 s20, s13\n")
+    assert not _hazards(body)
