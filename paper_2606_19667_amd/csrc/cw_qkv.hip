@@ -14,22 +14,31 @@
 //
 // Design (one workgroup = 8 wavefronts = one 256-feature x 256-token tile):
 //  * The product is formed as C^T = W x^T with v_mfma_f32_16x16x32_bf16:
-//    A = 16 rows of W, B = 16 token rows of x, 32 hidden per instruction (one
-//    pipeline step). In the 16x16 accumulator a lane holds one token and 4
-//    consecutive features, so everything the epilogue needs per element
-//    (position, block, slot) is per lane. This shape sustains a higher rate
-//    than 32x32x16 on random data (the card's power limit lowers the clock
-//    less for it).
+//    A = 16 rows of W, B = 16 token rows of x, 32 hidden per instruction. In
+//    the 16x16 accumulator a lane holds one token and 4 consecutive features,
+//    so everything the epilogue needs per element (position, block, slot) is
+//    per lane. This shape sustains a higher rate than 32x32x16 on random data
+//    (the card's power limit lowers the clock less for it).
 //  * Wave (wf, wt) owns features {j0 .. j0 + 31} and {j0 + D/2 .. + 31} of one
 //    head (four 16-row blocks) and 128 tokens (eight 16-token blocks). The
 //    blocks j0 + 16 p and j0 + D/2 + 16 p are exactly rotary pairs
 //    (j, j + D/2), which therefore sit in the same lane and register of two
 //    accumulators: the rotation needs no data exchange.
-//  * Hidden is walked in steps of 32. Four LDS stages of 32 KB (W rows then x
-//    rows, 64 bytes each) are filled by LDS-direct loads (global_load_lds,
-//    no registers), three steps ahead of their use; one barrier per step.
-//    The 16-byte chunk c of LDS row r holds global chunk c ^ ((r >> 2) & 3),
-//    so the 16 rows read by one operand phase hit distinct banks.
+//  * Hidden is walked in steps of 64 (two MFMA k-steps). Two LDS stages of
+//    64 KB (256 W rows then 256 x rows, 128 bytes each) are filled by
+//    LDS-direct loads (global_load_lds, no registers) one step ahead of their
+//    use; one barrier per step. Each load instruction brings 8 whole 128-byte
+//    rows (copies of whole lines out of L2 run at several times the rate of
+//    half-line copies). The 16-byte chunk c of LDS row r holds global chunk
+//    c ^ ((r >> 1) & 7), so the 16 rows read by one operand load hit distinct
+//    banks. An odd count of 32 hidden ends with a half step whose upper
+//    chunks are not used.
+//  * Within a step a wave loads the first k-step's operands, then issues its
+//    products in groups of one token block, each group followed by operand
+//    loads of the second k-step and one of the next step's copies; then the
+//    second k-step's products. The copies are inline asm, which the compiler
+//    does not track: tracked LDS-direct loads make it wait for every LDS read
+//    before the first product.
 //  * Tiles are numbered XCD-major (workgroup b runs on XCD b % 8), and within
 //    an XCD feature tiles vary fastest in groups of 8, so the workgroups that
 //    run together on one L2 share their W and x rows.
@@ -58,17 +67,20 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 constexpr int kThreads = 512;                  // 8 wavefronts
 constexpr int kTileF = 256;                    // output features per workgroup
 constexpr int kTileT = 256;                    // tokens per workgroup
-constexpr int kStep = 32;                      // hidden elements per pipeline step
-constexpr int kRow = kStep * 2;                // bytes of one staged row
-constexpr int kPart = kTileF * kRow;           // 16 KB: the W (or x) rows of a stage
-constexpr int kStage = 2 * kPart;
-constexpr int kStages = 4;
-constexpr int kAhead = kStages - 1;            // steps in flight
-constexpr int kCopies = 4;                     // 1 KB LDS-direct copies per wave and step
+constexpr int kStep = 64;                      // hidden elements per pipeline step
+constexpr int kRow = kStep * 2;                // bytes of one staged row (one 128-byte line)
+constexpr int kPartW = kTileF * kRow;          // 32 KB: the W rows of a stage
+constexpr int kStage = kPartW + kTileT * kRow; // + 16 KB of x rows
+constexpr int kStages = 2;
+constexpr int kAhead = kStages - 1;            // steps in flight (the loop's waits assume one)
+constexpr int kCopiesW = kPartW / 1024 / 8;    // 1 KB LDS-direct copies per wave and step: W rows
+constexpr int kCopiesX = kTileT * kRow / 1024 / 8;   // and x rows
+constexpr int kCopies = kCopiesW + kCopiesX;
 constexpr int kGroupF = 8;                     // feature tiles per XCD group
 constexpr int kBs = cw::kBlockSize;
-static_assert(kTileF == kTileT, "one staging layout serves W and x");
+static_assert(kCopiesW == 4 && kCopiesX == 4, "8 rows per copy, 32 W and 32 x rows per wave");
 static_assert(kStages * kStage <= 160 * 1024, "LDS of one CU");
+static_assert(kAhead == 1, "each step waits for all of its copies");
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
@@ -77,18 +89,21 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
 
-// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l. (Not in
-// the kernel template: the host pass of a template that names this builtin
-// directly emits no launch stub.)
+// One load-to-LDS copy: lane l's 16 bytes at src land at dst + 16 l (dst
+// wave-uniform, through M0). The compiler does not count it: the kernel's own
+// waits complete it.
 __device__ __forceinline__ void copy16_to_lds(const void* src, lds_void_t* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+  const uint32_t m = __builtin_amdgcn_readfirstlane(uint32_t(reinterpret_cast<uintptr_t>(dst)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(src), "s"(m) : "memory");
 }
 
 // s_waitcnt immediates (gfx9 encoding): vmcnt(n) with lgkmcnt(0), expcnt untouched.
 constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | (7 << 4) | ((n >> 4) << 14); }
 
-// Chunk swizzle of staged row r (64-byte rows, four 16-byte chunks).
-__device__ __forceinline__ int row_swz(int r) { return (r >> 2) & 3; }
+// Chunk swizzle of staged row r (128-byte rows, eight 16-byte chunks): the
+// 16 rows of an operand load, two per 256 bytes of banks, take 8 distinct
+// positions per row parity.
+__device__ __forceinline__ int row_swz(int r) { return (r >> 1) & 7; }
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -119,22 +134,33 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
   const int half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // ---- staging role: W rows and x rows 32 wave .. 32 wave + 31 of each step
+  // ---- staging role: W rows 32 wave .. + 31 and x rows 16 wave .. + 15 of
+  // each step; copy i brings 8 rows, lane l chunk l % 8 of row l / 8 (LDS
+  // position l % 8 holds global chunk (l % 8) ^ row_swz(row)).
   const int64_t hb = int64_t(hidden) * 2;   // bytes per row of W and x
   const uint8_t* src[kCopies];
+  int chunk[kCopies];
 #pragma unroll
   for (int i = 0; i < kCopies; ++i) {
-    const int row = 32 * wave + 16 * (i & 1) + (lane >> 2);
-    const int chunk = (lane & 3) ^ row_swz(row);
-    const uint8_t* base = (i < 2) ? w + int64_t(min(f0 + row, n_feat - 1)) * hb
-                                  : x + int64_t(min(t0 + row, T - 1)) * hb;
-    src[i] = base + chunk * 16;
+    const int row = i < kCopiesW ? 32 * wave + 8 * i + (lane >> 3) : 32 * wave + 8 * (i - kCopiesW) + (lane >> 3);
+    chunk[i] = (lane & 7) ^ row_swz(row);
+    src[i] = i < kCopiesW ? w + int64_t(min(f0 + row, n_feat - 1)) * hb : x + int64_t(min(t0 + row, T - 1)) * hb;
   }
+  const int nk = (hidden + kStep - 1) / kStep;
+  const bool half_last = (hidden % kStep) != 0;   // the last step holds 32 hidden
+  // copy i of a step into stage st
+  auto issue_one = [&](int step, int st, int i) __attribute__((always_inline)) {
+    uint8_t* dst = lds + st * kStage;
+    // (past the row's end in a half step the lane copies the chunk 4 below,
+    // which nothing reads)
+    const bool cut = half_last && step == nk - 1;
+    const int c = (cut && chunk[i] >= 4) ? chunk[i] - 4 : chunk[i];
+    const int off = i < kCopiesW ? (32 * wave + 8 * i) * kRow : kPartW + (32 * wave + 8 * (i - kCopiesW)) * kRow;
+    copy16_to_lds(src[i] + int64_t(step) * kRow + c * 16, (lds_void_t*)(dst + off));
+  };
   auto issue = [&](int step, int st) __attribute__((always_inline)) {
-    uint8_t* dst = lds + st * kStage + wave * 2048;
 #pragma unroll
-    for (int i = 0; i < kCopies; ++i)
-      copy16_to_lds(src[i] + int64_t(step) * kRow, (lds_void_t*)(dst + (i >> 1) * kPart + (i & 1) * 1024));
+    for (int i = 0; i < kCopies; ++i) issue_one(step, st, i);
   };
 
   // ---- operand rows of this wave
@@ -146,8 +172,10 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
   const int brow = wt * 128;
   const int l16 = lane & 15;
   const int g4 = lane >> 4;
-  // 16-row block starting at a multiple of 16 rows: lane reads row l16, chunk g4 (swizzled)
-  const int so = l16 * kRow + ((g4 ^ row_swz(l16)) << 4);
+  // 16-row block starting at a multiple of 16 rows, k-step ks of the stage:
+  // lane reads row l16, chunk 4 ks + g4 (swizzled)
+  const int so0 = l16 * kRow + ((g4 ^ row_swz(l16)) << 4);
+  const int so1 = l16 * kRow + (((4 + g4) ^ row_swz(l16)) << 4);
   // feature blocks: fa = 0, 1 -> j0 + 16 fa; fa = 2, 3 -> j0 + D/2 + 16 (fa - 2)
   int arow[4];
 #pragma unroll
@@ -159,35 +187,60 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
 #pragma unroll
     for (int tb = 0; tb < 8; ++tb) acc[fa][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = hidden / kStep;
 #pragma unroll
   for (int s = 0; s < kAhead; ++s)
     if (s < nk) issue(s, s);
 
   for (int k = 0; k < nk; ++k) {
-    const int later = min(nk - 1 - k, kAhead - 1);
-    if (later >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(2 * kCopies));
-    else if (later == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kCopies));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    // this step's copies have landed, in every wave; then the stage of step
+    // k - 1 is free for step k + 1
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (k + kAhead < nk) issue(k + kAhead, (k + kAhead) % kStages);
+    // the next step's copies go out with the first k-step's products (in the
+    // last step they copy that step's rows again into the free stage: the
+    // loop's end waits for them)
+    const int nxt = min(k + kAhead, nk - 1);
 
+    // The first k-step's operands, then its products in groups of one token
+    // block (4 MFMAs), each followed by loads of the second k-step's operands
+    // into the registers the group has consumed; then the second k-step's
+    // products. Scheduling barriers keep this order. A half step loads the
+    // second k-step's operands too and skips its products.
     const uint8_t* st = lds + (k % kStages) * kStage;
-    bf16x8 a[4], bx[8];
+    auto ld = [&](int row, int so) __attribute__((always_inline)) -> bf16x8 {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + row * kRow + so));
+    };
+    bf16x8 a0[4], a1[4], bx[8];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int fa = 0; fa < 4; ++fa)
-      a[fa] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + arow[fa] * kRow + so));
+    for (int fa = 0; fa < 4; ++fa) a0[fa] = ld(arow[fa], so0);
 #pragma unroll
-    for (int tb = 0; tb < 8; ++tb)
-      bx[tb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + kPart + (brow + 16 * tb) * kRow + so));
+    for (int tb = 0; tb < 8; ++tb) bx[tb] = ld(kTileF + brow + 16 * tb, so0);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int tb = 0; tb < 8; ++tb)
+    for (int tb = 0; tb < 8; ++tb) {
 #pragma unroll
       for (int fa = 0; fa < 4; ++fa)
-        acc[fa][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[fa], bx[tb], acc[fa][tb], 0, 0, 0);
+        acc[fa][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[fa], bx[tb], acc[fa][tb], 0, 0, 0);
+      bx[tb] = ld(kTileF + brow + 16 * tb, so1);
+      if (tb < 4) a1[tb] = ld(arow[tb], so1);
+      issue_one(nxt, (k + kAhead) % kStages, tb);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (!(half_last && k == nk - 1)) {
+#pragma unroll
+      for (int tb = 0; tb < 8; ++tb) {
+#pragma unroll
+        for (int fa = 0; fa < 4; ++fa)
+          acc[fa][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[fa], bx[tb], acc[fa][tb], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
   }
+
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
 
   // ---- epilogue: bias, rotation, bf16 rounding, stores
   const int hf = (f0 + head_l * D) / D;
@@ -283,7 +336,7 @@ extern "C" cw_status cw_qkv_rope_append(const void* x, const void* w, const void
   if (head_dim != 64 && head_dim != 128)
     return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": head_dim must be 64 or 128");
   if (block_size != kBs) return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": block_size must be 16");
-  if (hidden < kStep || hidden % kStep != 0 || hidden > (1 << 20))
+  if (hidden < kStep / 2 || hidden % (kStep / 2) != 0 || hidden > (1 << 20))
     return cw::fail(CW_EUNSUPPORTED, std::string(what) + ": hidden must be a multiple of 32 in [32, 2^20]");
   if (rope_len < 0) return cw::fail(CW_EINVAL, std::string(what) + ": rope_len must be >= 0");
   int64_t rows = 0;
