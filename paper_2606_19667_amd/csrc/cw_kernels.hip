@@ -904,14 +904,27 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) pb[kk] = __builtin_bit_cast(bf16x8, u32x4{w[4 * kk], w[4 * kk + 1], w[4 * kk + 2], w[4 * kk + 3]});
     };
-    // Where a step's copies go: the first half after MFMAs 0, E, 2E, .. of
-    // phase A, the second half likewise in phase B; a step without phase A
-    // (an entry's last) puts all of them in phase B.
+    // Where a step's copies go: the first half after MFMAs ke, ke + E, .. of
+    // phase A (ke: the groups before the wave's copy work), the second half
+    // after MFMAs 0, E, 2E, .. of phase B; a step without phase A (an entry's
+    // last) puts all of them in phase B.
+    // In the fused kernel waves 4-7 do their copy work after KS groups of
+    // phase A, waves 0-3 (and every wave of the other kernels) after kEarly:
+    // the two waves of a SIMD (w and w + 4) then take the CU's one scalar unit
+    // at different times, each while the other issues MFMAs. (The fused
+    // kernel's copy work is twice as long; for the others this measured
+    // slightly slower.)
     constexpr int HALF_C = LPW / 2;
     constexpr int kEarly = 2;   // phase A groups issued before a step's copy work
-    auto copies_a = [&](int i) __attribute__((always_inline)) {
-      constexpr int E = 2 * KS / HALF_C;
-      if (i % E == kEarly) copy_part(i / E);
+    constexpr int kLate = KS;   // (fused kernel, waves 4-7)
+    auto copies_a = [&](int i, int ke) __attribute__((always_inline)) {
+      if (ke == kEarly) {
+        constexpr int E = 2 * KS / HALF_C;
+        if (i % E == kEarly) copy_part(i / E);
+      } else {
+        constexpr int E = (2 * KS - kLate) / HALF_C;
+        if (i >= kLate && (i - kLate) % E == 0) copy_part((i - kLate) / E);
+      }
     };
     auto copies_b = [&](int i, bool all) __attribute__((always_inline)) {
       constexpr int E = 4 * DT / HALF_C, EA = 4 * DT / LPW;
@@ -935,7 +948,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
     // scalar copy work, so that the matrix pipe has work meanwhile); pack
     // ends the phase.
     auto phase_a = [&](int kb, int vb, bf16x8 (&kf)[3], bf16x8 (&vf)[3], const f32x16 (&sc)[2], f32x16 (&sn)[2],
-                       uint32_t (&w)[16], bf16x8 (&pb)[4], int i0, int i1, bool pack) __attribute__((always_inline)) {
+                       uint32_t (&w)[16], bf16x8 (&pb)[4], int i0, int i1, int ke, bool pack) __attribute__((always_inline)) {
       constexpr int N = 2 * KS;
       constexpr int PER = 16 / N;   // element pairs per MFMA (1 for D = 128, 2 for D = 64)
       __builtin_amdgcn_sched_barrier(0);
@@ -944,7 +957,7 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
         sn[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? mneg : sn[i & 1], 0, 0, 0);
         if (i + 3 < N) kf[i % 3] = rdk(kb, i + 3);
         else vf[i + 3 - N] = rdv(vb, i + 3 - N);
-        copies_a(i);
+        copies_a(i, ke);
 #pragma unroll
         for (int u = 0; u < PER; ++u) {
           w[i * PER + u] = prob_pair(sc, i * PER + u);
@@ -1154,9 +1167,16 @@ void suffix_prefill_attn_kernel(const AttnArgs a) {
       rebase(sc);
       bf16x8 pb[4];
       uint32_t w[16];
-      phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, 0, kEarly, false);
-      const bool direct = issue(p + kAhead, true);
-      phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, kEarly, 2 * KS, true);
+      bool direct;
+      if (!FUSED || wave < 4) {
+        phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, 0, kEarly, kEarly, false);
+        direct = issue(p + kAhead, true);
+        phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, kEarly, 2 * KS, kEarly, true);
+      } else {
+        phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, 0, kLate, kLate, false);
+        direct = issue(p + kAhead, true);
+        phase_a(kbase(p + 1), vbase(p), kf, vf, sc, sn, w, pb, kLate, 2 * KS, kLate, true);
+      }
       if (j + 1 >= n_full) mask(sn, (kbeg + j + 1) * kKv);
       mx = phase_b(vbase(p), vf, pb, sn);
       if (FUSED && j >= own_j0) step_barrier_w(direct, write_late(j));
