@@ -615,16 +615,20 @@ std::vector<Entry> plan_entries(const int32_t* cu, const int32_t* plen, int32_t 
     for (int32_t row0 = 0; row0 < S; row0 += per) {
       const int32_t nvalid = std::min(per, S - row0);
       const int32_t n = int32_t((int64_t(P) + row0 + nvalid + cw::kKvTile - 1) / cw::kKvTile);
-      const int32_t run = (n + splits - 1) / splits;
       for (int32_t g = 0; g < hkv; ++g)
         for (int32_t s = 0; s < splits; ++s) {
           Entry e;
-          const int32_t kb = std::min(n, s * run), ke = std::min(n, kb + run);
+          // run s: steps n s / splits .. n (s + 1) / splits - 1, so that the
+          // runs differ by at most one step and none is empty while n >= splits
+          const int32_t kb = int32_t(int64_t(n) * s / splits), ke = int32_t(int64_t(n) * (s + 1) / splits);
           // steps whose keys every row of the entry sees (key 64 k + 63 <= P + row0)
           const int32_t nfull = std::max(0, std::min(ke - kb, (P + row0 + 1) / cw::kKvTile - kb));
           const int32_t f[cw::kEntFields] = {r, g, row0, nvalid, cu[r], P, P + S, kb, ke, s, nfull, cu[r] + row0};
           std::copy(f, f + cw::kEntFields, e.f);
-          e.cost = (ke - kb) + (ke > kb ? kEntryOverhead : 0);
+          // (an empty run still writes its part and passes an entry switch:
+          // with cost 0, longest-first placement would stack every empty run
+          // on the least-loaded queue)
+          e.cost = (ke - kb) + kEntryOverhead;
           e.pair = r * hkv + g;
           out.push_back(e);
         }

@@ -195,8 +195,7 @@ def _check_plan(plan, cu, P, hq, hkv, splits=1):
         assert 0 <= g < hkv and row0 % per == 0 and nv == min(per, S - row0) and nv >= 1
         assert cu0 == cu[r] and p == P[r] and L == P[r] + S
         n = -(-(p + row0 + nv) // 64)
-        run = -(-n // splits)
-        assert 0 <= sp < splits and kb == min(n, sp * run) and ke == min(n, kb + run)
+        assert 0 <= sp < splits and kb == n * sp // splits and ke == n * (sp + 1) // splits
         runs.setdefault((r, g, row0), []).append((sp, kb, ke, n))
         if sp == 0:
             for row in range(row0, row0 + nv):
