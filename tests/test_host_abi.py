@@ -265,6 +265,28 @@ def test_plan_queues_are_balanced_longest_first():
     assert max(load.values()) <= min(load.values()) + heavy
 
 
+@pytest.mark.parametrize("splits", [6, 8, 16])
+def test_split_plan_spreads_empty_runs(splits):
+    """A single request with tiles of fewer steps than splits (some runs are
+    empty): the runs of a tile differ by at most one step, and the queues stay
+    balanced with an empty run counted as one step (regression: at cost 0
+    every empty run landed on one queue, 66 entries deep at 8 splits)."""
+    cu = np.array([0, 576], np.int32)
+    P = np.array([832], np.int32)
+    plan = cw.suffix_prefill_plan(cu, P, 32, 8, 128, splits)
+    _check_plan(plan, cu, P, 32, 8, splits)
+    per_tile = {}
+    for w, i, e in _entries(plan):
+        per_tile.setdefault((int(e[0]), int(e[1]), int(e[2])), []).append(int(e[cw.ENT_KEND] - e[cw.ENT_KBEG]))
+    for steps in per_tile.values():
+        assert max(steps) - min(steps) <= 1
+    n_entries = len(_entries(plan))
+    grid = int(plan[cw.HDR_GRID])
+    assert int(plan[cw.HDR_QUEUE_LEN]) <= -(-n_entries // grid) + 1
+    load, heavy = _queue_loads(plan)
+    assert max(load.values()) <= min(load.values()) + heavy
+
+
 def test_grouped_plan_runs_rounds_in_pair_order_and_stays_balanced():
     """With partition grouping, the entries a partition's queues hold at one
     queue position (a round, run at about the same time) are consecutive in
