@@ -602,9 +602,11 @@ def suffix_prefill_append_attn(meta: BatchMeta, q: torch.Tensor, k_new: torch.Te
 
 
 def split_count(meta: BatchMeta, num_cus: int = 256) -> int:
-    """A split count for cw_suffix_prefill_attn_split: enough runs that the
-    batch's tiles cover every CU at least once (one attention workgroup per CU)."""
-    return max(1, min(64, -(-num_cus // max(1, meta.num_tiles))))
+    """A split count for cw_suffix_prefill_attn_split: the most runs per tile
+    for which the batch's runs still fit one per CU (one attention workgroup
+    per CU): more would queue a second run on some CUs and lengthen the call
+    (1 when the tiles alone fill the CUs)."""
+    return max(1, min(64, num_cus // max(1, meta.num_tiles)))
 
 
 def split_workspace_bytes(meta: BatchMeta, num_splits: int) -> int:
