@@ -275,6 +275,19 @@ def config_points(seed: int, stream, names=("llama8b-single", "topk10-f0.0", "to
                          "achieved_TFLOPs": round(fl / sec / 1e12, 2),
                          "frac": round(fl / sec / 1e12 / PEAK_BF16_TFLOPS, 4),
                          "batch": int(S.size), "suffix_tokens": int(S.sum()), "prefix_tokens": int(P.sum())}
+        # a batch of fewer tiles than CUs: also the split-KV call (merge
+        # included) at the automatic split count
+        ns = cw.split_count(db.meta)
+        if ns > 1:
+            ws = torch.empty(cw.split_workspace_bytes(db.meta, ns), dtype=torch.uint8, device="cuda")
+            fs = lambda: cw.suffix_prefill_attn_split(db.meta, db.q, db.k_cache, db.v_cache, db.scale,
+                                                      num_splits=ns, workspace=ws, out=out, stream=stream)
+            for _ in range(10):
+                fs()
+            ts = percentiles_us(timed_calls(fs, stream, n))
+            out_all[name]["split"] = {"splits": ns, "tiles": int(db.meta.num_tiles), "attention_us": ts,
+                                      "frac": round(fl / (ts["median"] * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            del ws
         del db, out
         torch.cuda.empty_cache()
     return out_all
