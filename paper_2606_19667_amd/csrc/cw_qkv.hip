@@ -70,7 +70,7 @@ constexpr int kTileT = 256;                    // tokens per workgroup
 constexpr int kStep = 64;                      // hidden elements per pipeline step
 constexpr int kRow = kStep * 2;                // bytes of one staged row (one 128-byte line)
 constexpr int kPartW = kTileF * kRow;          // 32 KB: the W rows of a stage
-constexpr int kStage = kPartW + kTileT * kRow; // + 16 KB of x rows
+constexpr int kStage = kPartW + kTileT * kRow; // + 32 KB of x rows
 constexpr int kStages = 2;
 constexpr int kAhead = kStages - 1;            // steps in flight (the loop's waits assume one)
 constexpr int kCopiesW = kPartW / 1024 / 8;    // 1 KB LDS-direct copies per wave and step: W rows
@@ -134,7 +134,7 @@ void qkv_rope_append_kernel(const uint8_t* __restrict__ x, const uint8_t* __rest
   const int half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // ---- staging role: W rows 32 wave .. + 31 and x rows 16 wave .. + 15 of
+  // ---- staging role: W rows 32 wave .. + 31 and x rows 32 wave .. + 31 of
   // each step; copy i brings 8 rows, lane l chunk l % 8 of row l / 8 (LDS
   // position l % 8 holds global chunk (l % 8) ^ row_swz(row)).
   const int64_t hb = int64_t(hidden) * 2;   // bytes per row of W and x
